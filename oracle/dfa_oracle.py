@@ -1,0 +1,397 @@
+"""Plain fp64 CPU oracle for the DiTFastAttn attention hot path.
+
+TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+benchmark's CPU-baseline leg may import this module.  The product path (the
+HIP library and its Python binding) never calls it, and it shares no code,
+header, table or helper with that path.
+
+Everything here is the textbook definition written out in numpy float64, in
+the paper's order and notation (DiTFastAttn, arXiv 2406.08552):
+
+  * full attention            -- Sec. 3.2, Eq. (1) first line:  O = Attention(Q, K, V)
+  * window attention          -- Sec. 3.2 (attention restricted to a window along
+                                 the diagonal of the attention matrix), Eq. (1)-(2)
+  * WA-RS refresh             -- Sec. 3.2, Eq. (1):  R_r = O_r - W_r
+  * WA-RS reuse               -- Sec. 3.2, Eq. (2):  O_k = W_k + R_r
+  * AST                       -- Sec. 3.3: reuse the cached earliest-step output
+  * ASC                       -- Sec. 3.4: reuse the conditional half's output for
+                                 the unconditional half
+  * plan + cache bookkeeping  -- Sec. 3.5 / Alg. 1 output dictionary (per layer,
+                                 per step strategy); here drawn from a seeded
+                                 SplitMix64 stream instead of searched
+  * attention-FLOP accounting -- Table 2 ("Attn FLOPs" of the multi-head attention
+                                 module, window = 1/8 of the tokens, Sec. 4.1)
+
+Readings of points the paper leaves open (all listed with reasons in the
+design notes):
+  - the window is a 1D band over the flattened token index, |i - j| <= w,
+    symmetric and non-causal, truncated at 0 and L-1; w is the half-width;
+  - the softmax scale is 1/sqrt(d);
+  - AST returns the output of the layer's most recent non-AST step;
+  - a reuse step reads the residual of the layer's most recent refresh;
+  - in a CFG batch the first B/2 entries are conditional, entry b + B/2 is
+    the unconditional partner of entry b.
+
+Tensors are numpy arrays of shape [B, H, L, d] (float64).  Every function
+accepts any real dtype and computes in float64.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+# Plan codes (one per strategy a layer may run at a step).
+FULL, WARS_REFRESH, WARS_REUSE, AST_REUSE, ASC_REUSE = 0, 1, 2, 3, 4
+CODE_NAMES = {FULL: "FULL", WARS_REFRESH: "WARS_REFRESH", WARS_REUSE: "WARS_REUSE",
+              AST_REUSE: "AST_REUSE", ASC_REUSE: "ASC_REUSE"}
+
+_ROW_BLOCK = 1024  # query rows per block: bounds the fp64 score block at 1024 x L
+
+
+# ---------------------------------------------------------------------------
+# Window geometry (Sec. 3.2; window size 1/8 of the tokens, Sec. 4.1)
+# ---------------------------------------------------------------------------
+def band_mask(rows: np.ndarray, L: int, w: int) -> np.ndarray:
+    """Boolean [len(rows), L] mask of keys j with |i - j| <= w for each query i.
+
+    The band is truncated at the sequence ends (no wrap-around).  Every row
+    contains its own diagonal, so no row of the mask is empty."""
+    rows = np.asarray(rows, dtype=np.int64)
+    j = np.arange(L, dtype=np.int64)
+    return np.abs(rows[:, None] - j[None, :]) <= w
+
+
+def n_band(L: int, w: int) -> int:
+    """Number of (i, j) pairs with |i - j| <= w in an L x L attention matrix,
+    counted pair by pair (no closed form used here)."""
+    total = 0
+    for i in range(L):
+        lo = max(0, i - w)
+        hi = min(L - 1, i + w)
+        total += hi - lo + 1
+    return total
+
+
+# ---------------------------------------------------------------------------
+# Attention (Sec. 3.2 Eq. (1)-(2))
+# ---------------------------------------------------------------------------
+def _softmax_rows(S: np.ndarray, mask: np.ndarray | None) -> np.ndarray:
+    """Row softmax of a score block; masked-out entries get probability 0."""
+    if mask is not None:
+        S = np.where(mask, S, -np.inf)
+    m = np.max(S, axis=-1, keepdims=True)
+    E = np.exp(S - m)
+    return E / np.sum(E, axis=-1, keepdims=True)
+
+
+def attention_probs(q: np.ndarray, k: np.ndarray, w: int | None = None,
+                    rows: np.ndarray | None = None) -> np.ndarray:
+    """P = softmax(q k^T / sqrt(d)) for one (batch, head): q [Lq, d], k [L, d].
+
+    ``rows`` gives the token index of each query row (default 0..Lq-1); with
+    ``w`` set the softmax is restricted to the band |i - j| <= w."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    L, d = k.shape
+    if rows is None:
+        rows = np.arange(q.shape[0])
+    S = (q @ k.T) / np.sqrt(d)
+    mask = None if w is None else band_mask(rows, L, w)
+    return _softmax_rows(S, mask)
+
+
+def attention_rows(Q, K, V, rows, w: int | None = None) -> np.ndarray:
+    """Attention output for the query rows ``rows`` of every (batch, head).
+
+    Q, K, V: [B, H, L, d].  Returns [B, H, len(rows), d].  ``w=None`` is full
+    attention; an integer ``w`` is window attention over |i - j| <= w.  Both
+    take the same arithmetic path (the window is a mask on the same score
+    block), so a band that covers every key gives bit-identical results."""
+    Q = np.asarray(Q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    rows = np.asarray(rows, dtype=np.int64)
+    B, H, L, d = Q.shape
+    out = np.empty((B, H, len(rows), d), dtype=np.float64)
+    for b in range(B):
+        for h in range(H):
+            for r0 in range(0, len(rows), _ROW_BLOCK):
+                rr = rows[r0:r0 + _ROW_BLOCK]
+                P = attention_probs(Q[b, h, rr], K[b, h], w, rr)
+                out[b, h, r0:r0 + len(rr)] = P @ V[b, h]
+    return out
+
+
+def attn_full(Q, K, V) -> np.ndarray:
+    """O = softmax(Q K^T / sqrt(d)) V  (Eq. (1), first line)."""
+    L = np.shape(Q)[2]
+    return attention_rows(Q, K, V, np.arange(L), None)
+
+
+def attn_window(Q, K, V, w: int) -> np.ndarray:
+    """W = WindowAttention(Q, K, V): softmax over the keys with |i - j| <= w
+    only (Eq. (1) second line, Eq. (2) first line)."""
+    L = np.shape(Q)[2]
+    return attention_rows(Q, K, V, np.arange(L), w)
+
+
+# ---------------------------------------------------------------------------
+# WA-RS, AST, ASC (Sec. 3.2-3.4)
+# ---------------------------------------------------------------------------
+def wars_refresh(Q, K, V, w: int):
+    """First step r = min(K) of a residual-sharing set (Eq. (1)):
+    O_r = Attention, W_r = WindowAttention, R_r = O_r - W_r.
+    Returns (O_r, R_r)."""
+    O = attn_full(Q, K, V)
+    W = attn_window(Q, K, V, w)
+    return O, O - W
+
+
+def wars_reuse(Q, K, V, R, w: int) -> np.ndarray:
+    """Later step k of the set (Eq. (2)): O_k = W_k + R_r."""
+    return attn_window(Q, K, V, w) + np.asarray(R, dtype=np.float64)
+
+
+def ast_reuse(O_cache) -> np.ndarray:
+    """Attention sharing across timesteps (Sec. 3.3): the step's output is the
+    cached output of the earliest step of its set."""
+    return np.array(O_cache, dtype=np.float64, copy=True)
+
+
+def asc_reuse(Q, K, V) -> np.ndarray:
+    """Attention sharing across CFG (Sec. 3.4): attention is computed for the
+    conditional half of the batch (entries 0..B/2-1) and its output is reused
+    for the unconditional half (entry b + B/2 takes entry b's output)."""
+    B = np.shape(Q)[0]
+    if B % 2:
+        raise ValueError("ASC needs an even batch (conditional/unconditional pairs)")
+    half = B // 2
+    O_cond = attn_full(np.asarray(Q)[:half], np.asarray(K)[:half], np.asarray(V)[:half])
+    return np.concatenate([O_cond, O_cond], axis=0)
+
+
+# ---------------------------------------------------------------------------
+# Brute force (explicit loops) -- used only on tiny inputs, as an independent pin
+# ---------------------------------------------------------------------------
+def brute_force_attention(Q, K, V, w: int | None = None) -> np.ndarray:
+    """Explicit loops over (b, h, i, j) with math.exp; w=None is full attention."""
+    import math
+    Q = np.asarray(Q, dtype=np.float64)
+    K = np.asarray(K, dtype=np.float64)
+    V = np.asarray(V, dtype=np.float64)
+    B, H, L, d = Q.shape
+    out = np.zeros((B, H, L, d))
+    inv = 1.0 / math.sqrt(d)
+    for b in range(B):
+        for h in range(H):
+            for i in range(L):
+                keys = [j for j in range(L) if w is None or abs(i - j) <= w]
+                s = []
+                for j in keys:
+                    acc = 0.0
+                    for c in range(d):
+                        acc += Q[b, h, i, c] * K[b, h, j, c]
+                    s.append(acc * inv)
+                mx = max(s)
+                e = [math.exp(x - mx) for x in s]
+                z = sum(e)
+                for c in range(d):
+                    acc = 0.0
+                    for jj, j in enumerate(keys):
+                        acc += e[jj] / z * V[b, h, j, c]
+                    out[b, h, i, c] = acc
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Plan generator (stands in for the output dictionary of Alg. 1)
+# ---------------------------------------------------------------------------
+_MASK64 = (1 << 64) - 1
+
+
+class SplitMix64:
+    """SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): a Weyl sequence with
+    increment 0x9E3779B97F4A7C15 passed through a 64-bit finaliser."""
+
+    def __init__(self, seed: int):
+        self.state = seed & _MASK64
+
+    def next(self) -> int:
+        self.state = (self.state + 0x9E3779B97F4A7C15) & _MASK64
+        z = self.state
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _MASK64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _MASK64
+        return z ^ (z >> 31)
+
+
+def plan_make(seed: int, n_layers: int, n_steps: int, refresh_every: int, B: int):
+    """Seeded per-(step, layer) plan with legality repair.
+
+    Draw order is step-major (for t: for layer).  Each draw maps the high
+    32 bits of one SplitMix64 output to a code in 0..4 by multiply-shift.
+    Repairs, in order:
+      1. AST before the layer has any cached output        -> FULL
+      2. refresh_every > 0: a REFRESH or REUSE draw is "WA-RS" and becomes
+         REFRESH when the layer has no residual yet or its residual is
+         refresh_every or more steps old, else REUSE
+      3. refresh_every == 0: REUSE before any refresh       -> REFRESH
+      4. ASC with an odd batch                              -> ValueError
+    Returns int32 arrays [n_steps, n_layers]: executed code, r_src (the step
+    whose residual a REUSE reads, else -1) and o_src (the step whose output
+    the layer emits: t for computed steps, the cached step for AST)."""
+    if n_layers <= 0 or n_steps <= 0 or refresh_every < 0 or B <= 0:
+        raise ValueError("bad plan dimensions")
+    rng = SplitMix64(seed)
+    code = np.full((n_steps, n_layers), -1, dtype=np.int32)
+    r_src = np.full((n_steps, n_layers), -1, dtype=np.int32)
+    o_src = np.full((n_steps, n_layers), -1, dtype=np.int32)
+    last_refresh = [-1] * n_layers
+    cache_step = [-1] * n_layers
+    for t in range(n_steps):
+        for layer in range(n_layers):
+            c = ((rng.next() >> 32) * 5) >> 32
+            if c == AST_REUSE and cache_step[layer] < 0:
+                c = FULL
+            if refresh_every > 0 and c in (WARS_REFRESH, WARS_REUSE):
+                stale = last_refresh[layer] < 0 or t - last_refresh[layer] >= refresh_every
+                c = WARS_REFRESH if stale else WARS_REUSE
+            if refresh_every == 0 and c == WARS_REUSE and last_refresh[layer] < 0:
+                c = WARS_REFRESH
+            if c == ASC_REUSE and B % 2:
+                raise ValueError("ASC drawn with an odd batch")
+            code[t, layer] = c
+            if c == WARS_REUSE:
+                r_src[t, layer] = last_refresh[layer]
+            if c == AST_REUSE:
+                o_src[t, layer] = cache_step[layer]
+            else:
+                o_src[t, layer] = t
+                cache_step[layer] = t
+            if c == WARS_REFRESH:
+                last_refresh[layer] = t
+    return code, r_src, o_src
+
+
+def fixed_plan(codes, n_layers: int = 1):
+    """Source arrays for a caller-fixed code sequence (same cache rules as
+    plan_make, no repair): used by the tiny three-step check."""
+    n_steps = len(codes)
+    code = np.asarray(codes, dtype=np.int32).reshape(n_steps, 1).repeat(n_layers, 1)
+    r_src = np.full_like(code, -1)
+    o_src = np.full_like(code, -1)
+    for layer in range(n_layers):
+        last_refresh, cache_step = -1, -1
+        for t in range(n_steps):
+            c = int(code[t, layer])
+            if c == WARS_REUSE:
+                if last_refresh < 0:
+                    raise ValueError("reuse before any refresh")
+                r_src[t, layer] = last_refresh
+            if c == AST_REUSE:
+                if cache_step < 0:
+                    raise ValueError("AST before any cached output")
+                o_src[t, layer] = cache_step
+            else:
+                o_src[t, layer] = t
+                cache_step = t
+            if c == WARS_REFRESH:
+                last_refresh = t
+    return code, r_src, o_src
+
+
+class LayerCache:
+    """Per-layer state of the cache state machine: the residual of the latest
+    refresh (R) and the output of the latest non-AST step (O_cache)."""
+
+    def __init__(self):
+        self.R = None
+        self.O_cache = None
+
+
+def plan_step(code: int, Q, K, V, cache: LayerCache, w: int) -> np.ndarray:
+    """One layer at one step under the plan (Sec. 3.2-3.4):
+
+      FULL     O = Attention                       R unchanged   O_cache <- O
+      REFRESH  O = Attention, R = O - W            R <- O - W    O_cache <- O
+      REUSE    O = W + R                           R unchanged   O_cache <- O
+      AST      O = O_cache                         R unchanged   O_cache unchanged
+      ASC      O[cond] = Attention, O[uncond] = O[cond]          O_cache <- O
+    """
+    if code == FULL:
+        O = attn_full(Q, K, V)
+    elif code == WARS_REFRESH:
+        O, R = wars_refresh(Q, K, V, w)
+        cache.R = R
+    elif code == WARS_REUSE:
+        if cache.R is None:
+            raise ValueError("reuse before any refresh")
+        O = wars_reuse(Q, K, V, cache.R, w)
+    elif code == AST_REUSE:
+        if cache.O_cache is None:
+            raise ValueError("AST before any cached output")
+        return ast_reuse(cache.O_cache)
+    elif code == ASC_REUSE:
+        O = asc_reuse(Q, K, V)
+    else:
+        raise ValueError(f"unknown plan code {code}")
+    cache.O_cache = O
+    return O
+
+
+# ---------------------------------------------------------------------------
+# Sampled-row evaluation for long sequences
+# ---------------------------------------------------------------------------
+def plan_step_rows(code: int, Q, K, V, rows, cache: LayerCache, w: int) -> np.ndarray:
+    """plan_step restricted to the query rows ``rows`` (every batch entry and
+    head).  Attention rows are independent, so the per-row residual and output
+    caches carried here equal the corresponding rows of the full ones."""
+    rows = np.asarray(rows, dtype=np.int64)
+    if code == FULL:
+        O = attention_rows(Q, K, V, rows, None)
+    elif code == WARS_REFRESH:
+        O = attention_rows(Q, K, V, rows, None)
+        cache.R = O - attention_rows(Q, K, V, rows, w)
+    elif code == WARS_REUSE:
+        if cache.R is None:
+            raise ValueError("reuse before any refresh")
+        O = attention_rows(Q, K, V, rows, w) + cache.R
+    elif code == AST_REUSE:
+        if cache.O_cache is None:
+            raise ValueError("AST before any cached output")
+        return cache.O_cache.copy()
+    elif code == ASC_REUSE:
+        B = np.shape(Q)[0]
+        if B % 2:
+            raise ValueError("ASC needs an even batch")
+        half = B // 2
+        Oc = attention_rows(np.asarray(Q)[:half], np.asarray(K)[:half],
+                            np.asarray(V)[:half], rows, None)
+        O = np.concatenate([Oc, Oc], axis=0)
+    else:
+        raise ValueError(f"unknown plan code {code}")
+    cache.O_cache = O
+    return O
+
+
+# ---------------------------------------------------------------------------
+# Attention-FLOP accounting (Table 2)
+# ---------------------------------------------------------------------------
+def core_attention_flops(B: int, H: int, L: int, d: int, pairs: int | None = None) -> int:
+    """Multiply-add FLOPs of S = QK^T and O = PV over ``pairs`` (i, j) pairs
+    (default: all L*L): 2*d for the score and 2*d for the PV product."""
+    if pairs is None:
+        pairs = L * L
+    return 4 * B * H * d * pairs
+
+
+def module_attn_flops_fraction(L: int, D: int, w: int, share_cfg: bool) -> float:
+    """Attention-module FLOPs of WA-RS (reuse step) relative to the raw module.
+
+    The module is the QKV projection (3 * 2*L*D*D), the output projection
+    (2*L*D*D) and core attention over the hidden width D (4*D per pair).
+    WA-RS keeps the projections and restricts core attention to the band;
+    ASC halves everything (only the conditional half is computed)."""
+    proj = 8 * L * D * D
+    raw = proj + 4 * D * L * L
+    wars = proj + 4 * D * n_band(L, w)
+    frac = wars / raw
+    return frac / 2 if share_cfg else frac

@@ -1,0 +1,131 @@
+"""Seeded synthetic inputs for the attention hot path.
+
+This module only draws random numbers and rounds them to bf16; it contains
+none of the attention method's arithmetic.  Both sides of every parity check
+(the HIP library and the fp64 oracle) receive the same bf16 values from here.
+
+Recipe (stands in for the Q/K/V of a trained DiT; no dataset or weights):
+  * per (config, layer, tensor) an fp32 master X_0 ~ N(0, 1), drawn from
+    numpy PCG64 seeded with SeedSequence([240608552, cfg, layer, 0, tensor]),
+    tensor 0/1/2 = Q/K/V;
+  * drift per step: X_t = X_{t-1} + drift * N(0, 1), the step-t normals drawn
+    from SeedSequence([240608552, cfg, layer, t, tensor]);
+  * each use rounds X_t to bf16 (round to nearest even).
+For bench-scale tensors ``device_qkv`` draws on the device with torch's
+seeded generator instead (same distribution, different stream).
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+import torch
+
+SEED_BASE = 240608552
+
+
+@dataclass(frozen=True)
+class AttnConfig:
+    """One attention workload: shapes, band half-width and plan schedule."""
+    name: str
+    cfg_id: int
+    B: int
+    H: int
+    L: int
+    d: int
+    w: int
+    n_layers: int
+    n_steps: int
+    refresh_every: int
+    drift: float = 0.05
+    fp32_inputs: bool = False   # the tiny check draws fp32 masters
+
+    @property
+    def plan_seed(self) -> int:
+        return SEED_BASE + self.cfg_id
+
+
+# The five workloads: a tiny three-step check and four DiT / PixArt-Sigma
+# shaped attention layers (L = (resolution / 16)^2 tokens, H = 16, d = 72).
+CONFIGS = {
+    "tiny": AttnConfig("tiny_wars_check", 1, B=2, H=2, L=256, d=64, w=16,
+                       n_layers=1, n_steps=3, refresh_every=0, fp32_inputs=True),
+    "dit256": AttnConfig("dit_xl2_256px", 2, B=8, H=16, L=256, d=72, w=32,
+                         n_layers=28, n_steps=50, refresh_every=0),
+    "dit512": AttnConfig("dit_xl2_512px", 3, B=8, H=16, L=1024, d=72, w=128,
+                         n_layers=28, n_steps=50, refresh_every=0),
+    "pixart1k": AttnConfig("pixart_sigma_1024px", 4, B=2, H=16, L=4096, d=72, w=512,
+                           n_layers=28, n_steps=20, refresh_every=4),
+    "pixart2k": AttnConfig("pixart_sigma_2048px", 5, B=2, H=16, L=16384, d=72, w=2048,
+                           n_layers=28, n_steps=20, refresh_every=4),
+}
+
+
+def _normals(cfg_id: int, layer: int, step: int, tensor: int, shape) -> np.ndarray:
+    ss = np.random.SeedSequence([SEED_BASE, cfg_id, layer, step, tensor])
+    return np.random.Generator(np.random.PCG64(ss)).standard_normal(shape, dtype=np.float32)
+
+
+def master_qkv(cfg_id: int, layer: int, step: int, shape, drift: float = 0.05):
+    """fp32 masters (Q, K, V) of one layer at one step (random walk over steps)."""
+    out = []
+    for tensor in range(3):
+        x = _normals(cfg_id, layer, 0, tensor, shape)
+        for t in range(1, step + 1):
+            x = x + np.float32(drift) * _normals(cfg_id, layer, t, tensor, shape)
+        out.append(x)
+    return tuple(out)
+
+
+class DriftingQKV:
+    """Iterates the (Q, K, V) of one layer over steps 0, 1, 2, ... keeping the
+    fp32 masters, so step t costs one draw per tensor."""
+
+    def __init__(self, cfg_id: int, layer: int, shape, drift: float = 0.05):
+        self.cfg_id, self.layer, self.shape, self.drift = cfg_id, layer, tuple(shape), drift
+        self.step = -1
+        self.master = None
+
+    def advance(self):
+        self.step += 1
+        t = self.step
+        if t == 0:
+            self.master = [_normals(self.cfg_id, self.layer, 0, i, self.shape) for i in range(3)]
+        else:
+            self.master = [m + np.float32(self.drift) * _normals(self.cfg_id, self.layer, t, i, self.shape)
+                           for i, m in enumerate(self.master)]
+        return to_bf16(self.master)
+
+
+def to_bf16(arrays):
+    """Round fp32 arrays to bf16 (nearest even); returns CPU torch tensors."""
+    return tuple(torch.from_numpy(np.ascontiguousarray(a)).to(torch.bfloat16) for a in arrays)
+
+
+def as_f64(t: torch.Tensor) -> np.ndarray:
+    """The exact float64 value of a bf16 (or any) tensor, on the host."""
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def bf16_qkv(cfg_id: int, layer: int, step: int, shape, drift: float = 0.05):
+    """bf16 (Q, K, V) CPU tensors of one layer at one step."""
+    return to_bf16(master_qkv(cfg_id, layer, step, shape, drift))
+
+
+def device_qkv(seed: int, shape, device, n: int = 3):
+    """Bench-scale inputs: n bf16 N(0, 1) tensors drawn on ``device`` from a
+    torch generator seeded with ``seed``."""
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    return tuple(torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+                 .to(torch.bfloat16) for _ in range(n))
+
+
+def sample_rows(L: int, n: int, seed: int) -> np.ndarray:
+    """A sorted seeded sample of n distinct query rows out of L, always
+    including the first and last rows (the band's truncated edges)."""
+    if n >= L:
+        return np.arange(L)
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([SEED_BASE, 99, L, n, seed])))
+    inner = rng.choice(np.arange(1, L - 1), size=n - 2, replace=False)
+    return np.sort(np.concatenate([[0, L - 1], inner])).astype(np.int64)

@@ -1,0 +1,260 @@
+"""Pins that tie the fp64 oracle to facts fixed by the paper and by mathematics,
+independently of the oracle's own formulas.
+
+Each pin is a plain function that raises AssertionError on failure, so the
+same battery runs both as ordinary tests and against deliberately broken
+copies of the oracle (every planted mistake must trip at least one pin).
+"""
+from __future__ import annotations
+
+import math
+import os
+
+import numpy as np
+import torch
+
+from oracle import dfa_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _rand(shape, seed, scale=1.0):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    return rng.standard_normal(shape) * scale
+
+
+# P1 -- brute force: explicit loops over (b, h, i, j) with math.exp.
+def pin_brute_force(cases=((1, 2, 24, 8, (0, 1, 3, 23)), (1, 1, 20, 72, (0, 2, 19)),
+                           (2, 1, 17, 64, (1, 4)))):
+    for B, H, L, d, ws in cases:
+        Q, K, V = (_rand((B, H, L, d), s) for s in (1, 2, 3))
+        bf = O.brute_force_attention(Q, K, V, None)
+        assert np.max(np.abs(O.attn_full(Q, K, V) - bf)) <= 1e-12
+        for w in ws:
+            bw = O.brute_force_attention(Q, K, V, w)
+            assert np.max(np.abs(O.attn_window(Q, K, V, w) - bw)) <= 1e-12
+            _, R = O.wars_refresh(Q, K, V, w)
+            assert np.max(np.abs(R - (bf - bw))) <= 1e-12
+
+
+# P2 -- library reduction: torch's scaled_dot_product_attention on the CPU in
+# float64 with a boolean band mask (True = attend).
+def pin_torch_sdpa(cases=((2, 3, 67, 72, (0, 5, 8, 66)), (1, 2, 130, 64, (16, 129)))):
+    for B, H, L, d, ws in cases:
+        Q, K, V = (_rand((B, H, L, d), s + 10) for s in (1, 2, 3))
+        tq, tk, tv = (torch.from_numpy(x) for x in (Q, K, V))
+        ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv).numpy()
+        assert np.max(np.abs(O.attn_full(Q, K, V) - ref)) <= 1e-12
+        i = torch.arange(L)
+        for w in ws:
+            mask = (i[:, None] - i[None, :]).abs() <= w
+            ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask).numpy()
+            assert np.max(np.abs(O.attn_window(Q, K, V, w) - ref)) <= 1e-12
+
+
+# P3 -- a band that covers every key is full attention: W == O bitwise, R == 0.
+def pin_wide_band():
+    Q, K, V = (_rand((1, 2, 40, 16), s + 20) for s in (1, 2, 3))
+    Of = O.attn_full(Q, K, V)
+    for w in (39, 40, 1000):
+        assert np.array_equal(O.attn_window(Q, K, V, w), Of)
+        Or, R = O.wars_refresh(Q, K, V, w)
+        assert np.array_equal(Or, Of) and not np.any(R)
+
+
+# P4 -- w = 0: each query attends only to itself, W = V.
+def pin_zero_band():
+    Q, K, V = (_rand((2, 2, 33, 72), s + 30) for s in (1, 2, 3))
+    W = O.attn_window(Q, K, V, 0)
+    assert np.max(np.abs(W - V)) <= 1e-15 * np.max(np.abs(V))
+
+
+# P5 -- Q = 0: uniform weights; O is the mean of V over all keys and W the
+# mean of V over the truncated band [max(0, i-w), min(L-1, i+w)].
+def pin_zero_query():
+    B, H, L, d = 1, 2, 50, 24
+    Q = np.zeros((B, H, L, d))
+    K, V = _rand((B, H, L, d), 41), _rand((B, H, L, d), 42)
+    Of = O.attn_full(Q, K, V)
+    assert np.max(np.abs(Of - V.mean(axis=2, keepdims=True))) <= 1e-13
+    for w in (0, 3, 12, 49):
+        W = O.attn_window(Q, K, V, w)
+        for i in range(L):
+            lo, hi = max(0, i - w), min(L - 1, i + w)
+            assert np.max(np.abs(W[:, :, i] - V[:, :, lo:hi + 1].mean(axis=2))) <= 1e-13
+
+
+# P6 -- constant value rows: every convex combination of c is c.
+def pin_constant_values():
+    B, H, L, d = 2, 1, 29, 8
+    Q, K = _rand((B, H, L, d), 51, 3.0), _rand((B, H, L, d), 52, 3.0)
+    c = _rand((d,), 53)
+    V = np.broadcast_to(c, (B, H, L, d)).copy()
+    for out in (O.attn_full(Q, K, V), O.attn_window(Q, K, V, 4)):
+        assert np.max(np.abs(out - c)) <= 1e-14
+
+
+# P7 -- probabilities: nonnegative, rows sum to one, zero outside the band,
+# and proportional to exp(q.k / sqrt(d)) inside it.
+def pin_probabilities():
+    L, d, w = 37, 16, 5
+    q, k = _rand((L, d), 61, 2.0), _rand((L, d), 62, 2.0)
+    for ww in (None, w):
+        P = O.attention_probs(q, k, ww)
+        assert np.all(P >= 0)
+        assert np.max(np.abs(P.sum(axis=1) - 1)) <= 1e-12
+        i = 3
+        j = np.arange(L) if ww is None else np.arange(max(0, i - ww), min(L, i + ww + 1))
+        ratio = P[i, j] / np.exp(q[i] @ k[j].T / math.sqrt(d))
+        assert np.max(np.abs(ratio / ratio[0] - 1)) <= 1e-12
+    P = O.attention_probs(q, k, w)
+    ii, jj = np.meshgrid(np.arange(L), np.arange(L), indexing="ij")
+    assert not np.any(P[np.abs(ii - jj) > w])
+    assert np.all(P[np.abs(ii - jj) <= w] > 0)
+
+
+# P8 -- zero drift: a reuse step at unchanged inputs rebuilds the refresh
+# step's full-attention output (Eq. (1) and (2) together).
+def pin_refresh_reuse_algebra():
+    Q, K, V = (_rand((2, 2, 45, 72), s + 70) for s in (1, 2, 3))
+    for w in (0, 4, 11):
+        Of, R = O.wars_refresh(Q, K, V, w)
+        assert np.max(np.abs(Of - O.attn_full(Q, K, V))) <= 1e-15
+        assert np.max(np.abs(O.wars_reuse(Q, K, V, R, w) - Of)) <= 1e-12
+        assert np.max(np.abs(R)) > 1e-6  # a narrow band really loses mass
+
+
+# P9 -- ASC: the conditional half is full attention on that half and the
+# unconditional half is a bit-identical copy; AST returns the cache bitwise;
+# the cache state machine follows its table.
+def pin_sharing():
+    B, H, L, d, w = 4, 2, 30, 16, 3
+    Q, K, V = (_rand((B, H, L, d), s + 80) for s in (1, 2, 3))
+    Oa = O.asc_reuse(Q, K, V)
+    assert np.array_equal(Oa[:B // 2], Oa[B // 2:])
+    assert np.array_equal(Oa[:B // 2], O.attn_full(Q[:B // 2], K[:B // 2], V[:B // 2]))
+    assert not np.array_equal(Oa[B // 2:], O.attn_full(Q[B // 2:], K[B // 2:], V[B // 2:]))
+    cache = O.LayerCache()
+    O0 = O.plan_step(O.WARS_REFRESH, Q, K, V, cache, w)
+    R0 = cache.R.copy()
+    Q2, K2, V2 = Q + 0.05 * _rand(Q.shape, 91), K + 0.05 * _rand(Q.shape, 92), V + 0.05 * _rand(Q.shape, 93)
+    O1 = O.plan_step(O.WARS_REUSE, Q2, K2, V2, cache, w)
+    assert np.array_equal(cache.R, R0) and np.array_equal(cache.O_cache, O1)
+    assert np.max(np.abs(O1 - (O.attn_window(Q2, K2, V2, w) + R0))) <= 1e-15
+    O2 = O.plan_step(O.AST_REUSE, Q, K, V, cache, w)
+    assert np.array_equal(O2, O1) and np.array_equal(cache.O_cache, O1)
+    O3 = O.plan_step(O.FULL, Q2, K2, V2, cache, w)
+    assert np.array_equal(cache.R, R0) and np.array_equal(cache.O_cache, O3)
+    assert not np.array_equal(O0, O1)
+
+
+# P10 -- a joint permutation of key/value rows leaves full attention
+# unchanged and changes window attention (the band is positional).
+def pin_permutation():
+    B, H, L, d, w = 1, 2, 41, 16, 4
+    Q, K, V = (_rand((B, H, L, d), s + 100) for s in (1, 2, 3))
+    perm = np.random.Generator(np.random.PCG64(7)).permutation(L)
+    Kp, Vp = K[:, :, perm], V[:, :, perm]
+    assert np.max(np.abs(O.attn_full(Q, Kp, Vp) - O.attn_full(Q, K, V))) <= 1e-12
+    assert np.max(np.abs(O.attn_window(Q, Kp, Vp, w) - O.attn_window(Q, K, V, w))) > 1e-3
+
+
+# P11 -- Table 2 "Attn FLOPs": WA-RS and WA-RS+ASC fractions of the attention
+# module at L = 1024/4096/16384 with the window 1/8 of the tokens read as the
+# half-width w = L/8, truncated at the sequence ends.  The band size comes
+# from the oracle's own mask, counted row by row.
+def load_t2():
+    rows = []
+    with open(os.path.join(GOLDEN, "t2_attn_flops.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                name, L, asc, wars, wars_asc, ast = line.split()
+                rows.append((name, int(L), int(asc), int(wars), int(wars_asc), int(ast)))
+    return rows
+
+
+def _mask_pairs(L, w):
+    total = 0
+    for r0 in range(0, L, 2048):
+        total += int(O.band_mask(np.arange(r0, min(L, r0 + 2048)), L, w).sum())
+    return total
+
+
+def pin_table2(D=1152):
+    rows = load_t2()
+    assert len(rows) == 3
+    exact = 0
+    for _, L, asc, wars, wars_asc, ast in rows:
+        w = L // 8
+        pairs = O.n_band(L, w)
+        assert pairs == _mask_pairs(L, w)
+        assert pairs == L * (2 * w + 1) - w * (w + 1)  # closed form of the truncated band
+        f = 100 * O.module_attn_flops_fraction(L, D, w, share_cfg=False)
+        f2 = 100 * O.module_attn_flops_fraction(L, D, w, share_cfg=True)
+        # every printed cell within one point; five of the six within rounding
+        # (the DiT-512 WA-RS cell computes to 76.47 against a printed 77)
+        assert abs(f - wars) <= 1.0, (L, f, wars)
+        assert abs(f2 - wars_asc) <= 1.0, (L, f2, wars_asc)
+        exact += (abs(f - wars) <= 0.5) + (abs(f2 - wars_asc) <= 0.5)
+        assert asc == 50 and ast == 0
+        # the other reading (total width L/8, i.e. half-width L/16) misses the table
+        g = 100 * O.module_attn_flops_fraction(L, D, L // 16, share_cfg=False)
+        assert abs(g - wars) > 2.0
+    assert exact >= 5
+
+
+# P12 -- plan generator: SplitMix64 known answers, legality invariants.
+# Known answers of the published SplitMix64 reference implementation
+# (splitmix64.c), seed 1234567, first five outputs.
+SPLITMIX64_KAT = (6457827717110365317, 3203168211198807973, 9817491932198370423,
+                  4593380528125082431, 16408922859458223821)
+
+
+def pin_plan():
+    r = O.SplitMix64(1234567)
+    assert tuple(r.next() for _ in range(5)) == SPLITMIX64_KAT
+    hist = np.zeros(5, dtype=np.int64)
+    for seed in range(40):
+        r = O.SplitMix64(seed)
+        for _ in range(200):
+            hist[((r.next() >> 32) * 5) >> 32] += 1
+    assert hist.min() > 0.9 * hist.mean() and hist.max() < 1.1 * hist.mean()
+    for seed, n_layers, n_steps, every, B in ((5, 28, 50, 0, 8), (6, 28, 20, 4, 2), (7, 3, 40, 2, 2),
+                                              (8, 5, 30, 0, 4)):
+        check_plan_invariants(*O.plan_make(seed, n_layers, n_steps, every, B), every)
+    code, _, _ = O.plan_make(1, 28, 50, 0, 8)
+    assert set(np.unique(code)) == {0, 1, 2, 3, 4}
+
+
+def check_plan_invariants(code, r_src, o_src, refresh_every):
+    n_steps, n_layers = code.shape
+    for layer in range(n_layers):
+        last_refresh, cache_step = -1, -1
+        for t in range(n_steps):
+            c = code[t, layer]
+            assert 0 <= c <= 4
+            if t == 0:
+                assert c != O.AST_REUSE
+            if c == O.WARS_REUSE:
+                assert r_src[t, layer] == last_refresh >= 0
+                if refresh_every > 0:
+                    assert 0 <= t - r_src[t, layer] < refresh_every
+            else:
+                assert r_src[t, layer] == -1
+            if c == O.WARS_REFRESH and refresh_every > 0 and last_refresh >= 0:
+                assert t - last_refresh >= refresh_every
+            if c == O.AST_REUSE:
+                assert o_src[t, layer] == cache_step and 0 <= cache_step < t
+            else:
+                assert o_src[t, layer] == t
+                cache_step = t
+            if c == O.WARS_REFRESH:
+                last_refresh = t
+
+
+ALL_PINS = {
+    "P1": pin_brute_force, "P2": pin_torch_sdpa, "P3": pin_wide_band, "P4": pin_zero_band,
+    "P5": pin_zero_query, "P6": pin_constant_values, "P7": pin_probabilities,
+    "P8": pin_refresh_reuse_algebra, "P9": pin_sharing, "P10": pin_permutation,
+    "P11": pin_table2, "P12": pin_plan,
+}

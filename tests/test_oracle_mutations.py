@@ -1,0 +1,161 @@
+"""Planted mistakes in the oracle must each trip at least one pin.
+
+Every mutation replaces one oracle function with a plausibly wrong variant
+(a dropped or wrong term, an off-by-one, a transposed operand, a flipped
+sign); the pin battery then has to fail.  Runs on the CPU only.
+"""
+import numpy as np
+import pytest
+
+from oracle import dfa_oracle as O
+from tests import oracle_pins as pins
+
+# cheap pins first: a mutation stops at the first pin that catches it
+ORDER = ["P4", "P3", "P6", "P7", "P5", "P8", "P9", "P10", "P12", "P2", "P1", "P11"]
+
+
+def _probs_factory(scale_fn=None, transpose=False, axis=-1):
+    def probs(q, k, w=None, rows=None):
+        q = np.asarray(q, dtype=np.float64)
+        k = np.asarray(k, dtype=np.float64)
+        L, d = k.shape
+        if rows is None:
+            rows = np.arange(q.shape[0])
+        S = (q @ k.T) * (scale_fn(d) if scale_fn else 1.0 / np.sqrt(d))
+        if transpose:
+            S = S.T[:q.shape[0]] if S.shape[0] == S.shape[1] else S
+        mask = None if w is None else O.band_mask(rows, L, w)
+        if mask is not None:
+            S = np.where(mask, S, -np.inf)
+        E = np.exp(S - np.max(S, axis=-1, keepdims=True))
+        return E / np.sum(E, axis=axis, keepdims=True)
+    return probs
+
+
+def _band_strict(rows, L, w):
+    j = np.arange(L)
+    return np.abs(np.asarray(rows)[:, None] - j[None, :]) < w
+
+
+def _band_wrap(rows, L, w):
+    j = np.arange(L)
+    dist = np.abs(np.asarray(rows)[:, None] - j[None, :])
+    return np.minimum(dist, L - dist) <= w
+
+
+def _band_shifted(rows, L, w):
+    # constant-width window slid inward at the sequence ends
+    rows = np.asarray(rows)
+    lo = np.clip(rows - w, 0, max(0, L - 1 - 2 * w))
+    j = np.arange(L)
+    return (j[None, :] >= lo[:, None]) & (j[None, :] <= lo[:, None] + 2 * w)
+
+
+def _n_band_no_trunc(L, w):
+    return L * (2 * w + 1)
+
+
+def _refresh_sign(Q, K, V, w):
+    Of = O.attn_full(Q, K, V)
+    return Of, O.attn_window(Q, K, V, w) - Of
+
+
+def _reuse_on_full(Q, K, V, R, w):
+    return O.attn_full(Q, K, V) + R
+
+
+def _asc_uncond_source(Q, K, V):
+    half = np.shape(Q)[0] // 2
+    Ou = O.attn_full(np.asarray(Q)[half:], np.asarray(K)[half:], np.asarray(V)[half:])
+    return np.concatenate([Ou, Ou], axis=0)
+
+
+_orig_plan_step = O.plan_step
+
+
+def _plan_step_full_clears_R(code, Q, K, V, cache, w):
+    out = _orig_plan_step(code, Q, K, V, cache, w)
+    if code == O.FULL:
+        cache.R = None if cache.R is None else np.zeros_like(cache.R)
+    return out
+
+
+_orig_plan_make = O.plan_make
+
+
+class _SplitMixTypo(O.SplitMix64):
+    def next(self):
+        self.state = (self.state + 0x9E3779B97F4A7C15) & O._MASK64
+        z = self.state
+        z = ((z ^ (z >> 31)) * 0xBF58476D1CE4E5B9) & O._MASK64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & O._MASK64
+        return z ^ (z >> 31)
+
+
+def _plan_age_off_by_one(seed, n_layers, n_steps, refresh_every, B):
+    rng = O.SplitMix64(seed)
+    code = np.full((n_steps, n_layers), -1, dtype=np.int32)
+    r_src = np.full_like(code, -1)
+    o_src = np.full_like(code, -1)
+    last, cache = [-1] * n_layers, [-1] * n_layers
+    for t in range(n_steps):
+        for l in range(n_layers):
+            c = ((rng.next() >> 32) * 5) >> 32
+            if c == O.AST_REUSE and cache[l] < 0:
+                c = O.FULL
+            if refresh_every > 0 and c in (1, 2):
+                c = 1 if (last[l] < 0 or t - last[l] > refresh_every) else 2  # '>' for '>='
+            if refresh_every == 0 and c == 2 and last[l] < 0:
+                c = 1
+            code[t, l] = c
+            if c == 2:
+                r_src[t, l] = last[l]
+            if c == 3:
+                o_src[t, l] = cache[l]
+            else:
+                o_src[t, l] = t
+                cache[l] = t
+            if c == 1:
+                last[l] = t
+    return code, r_src, o_src
+
+
+def _plan_ast_at_start(seed, n_layers, n_steps, refresh_every, B):
+    code, r_src, o_src = _orig_plan_make(seed, n_layers, n_steps, refresh_every, B)
+    code = code.copy()
+    code[0, 0] = O.AST_REUSE
+    return code, r_src, o_src
+
+
+MUTATIONS = {
+    "scale_1_over_d": ("attention_probs", _probs_factory(scale_fn=lambda d: 1.0 / d)),
+    "scale_missing": ("attention_probs", _probs_factory(scale_fn=lambda d: 1.0)),
+    "scores_transposed": ("attention_probs", _probs_factory(transpose=True)),
+    "softmax_wrong_axis": ("attention_probs", _probs_factory(axis=0)),
+    "band_strict": ("band_mask", _band_strict),
+    "band_wraps": ("band_mask", _band_wrap),
+    "band_shifted_at_edges": ("band_mask", _band_shifted),
+    "band_count_untruncated": ("n_band", _n_band_no_trunc),
+    "residual_sign": ("wars_refresh", _refresh_sign),
+    "reuse_adds_to_full": ("wars_reuse", _reuse_on_full),
+    "asc_wrong_half": ("asc_reuse", _asc_uncond_source),
+    "full_clears_residual": ("plan_step", _plan_step_full_clears_R),
+    "splitmix_shift_typo": ("SplitMix64", _SplitMixTypo),
+    "refresh_age_off_by_one": ("plan_make", _plan_age_off_by_one),
+    "ast_at_first_step": ("plan_make", _plan_ast_at_start),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_mutation_is_caught(name, monkeypatch):
+    attr, repl = MUTATIONS[name]
+    monkeypatch.setattr(O, attr, repl)
+    caught = None
+    for pin in ORDER:
+        try:
+            with np.errstate(all="ignore"):
+                pins.ALL_PINS[pin]()
+        except (AssertionError, ValueError, FloatingPointError, IndexError):
+            caught = pin
+            break
+    assert caught is not None, f"planted mistake {name!r} passed every pin"
