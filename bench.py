@@ -1,0 +1,246 @@
+"""Benchmark of the DiTFastAttn attention hot path on one MI355X.
+
+One step = one pass of the whole hot path: the seeded per-(step, layer) plan
+of the PixArt-Sigma 2K-shaped workload (B=2 as one CFG pair, H=16, L=16384
+tokens, d=72, band half-width w=2048, 28 layers x 20 denoising steps, WA-RS
+refreshed every 4 steps) executed through dfa_plan_step: full attention,
+WA-RS refresh and reuse, AST and ASC entries as the plan dictates.  Inputs
+(per-layer Q/K/V, bf16 N(0,1)) and the per-layer residual/output caches are
+resident in HBM before the timed region.
+
+Printed: one JSON line.  `value` is the executed algorithmic attention
+throughput of the plan run (FULL/REFRESH 4*B*H*L^2*d, REUSE 4*B*H*d*N_band,
+ASC 2*B*H*L^2*d, AST 0 FLOPs per layer-step) in TFLOP/s.  Also reported:
+ms per layer-step of the plan run and of a full-attention-only run on the
+same inputs, per-kernel times, the roofline of the dominant kernel (the full
+attention kernel, measured with HIP events on its launch stream inside the
+timed region) and the fp64 CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "bf16 attention TFLOP/s + ms/layer-step, full vs WA-RS, L=16384 H=16 d=72"
+
+
+def n_band(L: int, w: int) -> int:
+    if w >= L - 1:
+        return L * L
+    return L * (2 * w + 1) - w * (w + 1)
+
+
+def code_flops(code: int, B: int, H: int, L: int, d: int, w: int) -> float:
+    full = 4.0 * B * H * L * L * d
+    return {0: full, 1: full, 2: 4.0 * B * H * d * n_band(L, w), 3: 0.0, 4: full / 2}[code]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="pixart2k", choices=["pixart2k", "pixart1k", "dit512", "dit256"])
+    ap.add_argument("--kernel-reps", type=int, default=10)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(cfg, target_s: float):
+    """The fp64 oracle (as it is) on a bounded sample of one FULL layer-step:
+    every (batch, head) for a seeded sample of query rows, sized to about
+    target_s seconds of host work, scaled to TFLOP/s."""
+    import numpy as np
+
+    from oracle import dfa_oracle as orc
+    from paper_2406_08552_amd import inputs
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"),
+                      default=1)
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    B, H, L, d = cfg.B, cfg.H, cfg.L, cfg.d
+    rng = np.random.Generator(np.random.PCG64(inputs.SEED_BASE + 7))
+    # one layer's Q/K/V rounded to bf16, as the GPU sees them
+    import torch
+    Q, K, V = (torch.from_numpy(rng.standard_normal((B, H, L, d), dtype=np.float32)).to(torch.bfloat16)
+               .to(torch.float64).numpy() for _ in range(3))
+    n_rows, elapsed, flops = 16, 0.0, 0.0
+    while True:
+        rows = inputs.sample_rows(L, n_rows, 3)
+        t0 = time.perf_counter()
+        orc.attention_rows(Q, K, V, rows, None)
+        elapsed = time.perf_counter() - t0
+        flops = 4.0 * B * H * len(rows) * L * d
+        if elapsed >= target_s / 4 or n_rows >= L:
+            break
+        n_rows = min(L, n_rows * 4 if elapsed < target_s / 16 else n_rows * 2)
+    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"full attention of {len(rows)} seeded query rows x all {B * H} (batch, head) pairs of one "
+                      f"L={L} d={d} layer-step, fp64 numpy, {elapsed:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1"}), flush=True)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2406_08552_amd import dfa, inputs
+
+    cfg = inputs.CONFIGS[args.workload]
+    B, H, L, d, w = cfg.B, cfg.H, cfg.L, cfg.d, cfg.w
+    NL, NS = cfg.n_layers, cfg.n_steps
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    shape = (B, H, L, d)
+
+    code, r_src, o_src = dfa.dfa_plan_make(cfg.plan_seed, NL, NS, cfg.refresh_every, B)
+
+    # resident inputs and per-layer caches (the output buffer is the AST cache)
+    qkv = [inputs.device_qkv(inputs.SEED_BASE + 1000 * cfg.cfg_id + l, shape, dev) for l in range(NL)]
+    O = [torch.empty(shape, dtype=torch.bfloat16, device=dev) for _ in range(NL)]
+    R = [torch.empty(shape, dtype=torch.float32, device=dev) for _ in range(NL)]
+    torch.cuda.synchronize()
+
+    def plan_pass(codes, events=None):
+        for t in range(NS):
+            for l in range(NL):
+                c = int(codes[t, l])
+                q, k, v = qkv[l]
+                if events is not None:
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                dfa.dfa_plan_step(c, q, k, v, O[l], R[l], O[l], w, stream)
+                if events is not None:
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e1.record(stream)
+                    events.append((c, e0, e1))
+
+    for _ in range(args.warmup):
+        plan_pass(code)
+    torch.cuda.synchronize()
+
+    # timed region: K plan passes
+    events = []
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for _ in range(args.steps):
+        plan_pass(code, events)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    gpu_ms = t_start.elapsed_time(t_end)
+    ms_per_step = max(gpu_ms, wall * 1e3) / args.steps
+
+    per_code = {}
+    for c, e0, e1 in events:
+        per_code.setdefault(c, []).append(e0.elapsed_time(e1))
+    flops_per_pass = sum(code_flops(int(c), B, H, L, d, w) for c in code.flat)
+    value = flops_per_pass / (ms_per_step * 1e-3) / 1e12
+
+    # full-attention-only run on the same inputs (the uncompressed baseline)
+    full_codes = code.copy()
+    full_codes[:] = dfa.FULL
+    plan_pass(full_codes)
+    torch.cuda.synchronize()
+    f0 = time.perf_counter()
+    fs = torch.cuda.Event(enable_timing=True)
+    fe = torch.cuda.Event(enable_timing=True)
+    fs.record(stream)
+    plan_pass(full_codes)
+    fe.record(stream)
+    torch.cuda.synchronize()
+    full_only_ms = max(fs.elapsed_time(fe), (time.perf_counter() - f0) * 1e3)
+
+    # per-kernel times at the same shape (each entry point on its own)
+    q, k, v = qkv[0]
+    Ok = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+    Rk = torch.empty(shape, dtype=torch.float32, device=dev)
+    Ck = torch.empty_like(Ok)
+    dfa.dfa_attn_full_and_residual(q, k, v, Ok, Rk, w, stream)
+    kernels = {
+        "full": (lambda: dfa.dfa_attn_full(q, k, v, Ok, w, stream), code_flops(0, B, H, L, d, w), 4),
+        "wars_refresh": (lambda: dfa.dfa_attn_full_and_residual(q, k, v, Ok, Rk, w, stream),
+                         code_flops(1, B, H, L, d, w), 6),
+        "wars_reuse": (lambda: dfa.dfa_attn_window_plus_residual(q, k, v, Ok, Rk, w, stream),
+                       code_flops(2, B, H, L, d, w), 6),
+        "asc": (lambda: dfa.dfa_plan_step(dfa.ASC_REUSE, q, k, v, Ok, None, None, w, stream),
+                code_flops(4, B, H, L, d, w), 2.5),
+        "ast_copy": (lambda: dfa.dfa_plan_step(dfa.AST_REUSE, None, None, None, Ok, None, Ck, w, stream), 0.0, 2),
+    }
+    tensor_bytes = B * H * L * d * 2
+    kres = {}
+    for name, (fn, fl, ntens) in kernels.items():
+        fn()
+        torch.cuda.synchronize()
+        s0 = torch.cuda.Event(enable_timing=True)
+        s1 = torch.cuda.Event(enable_timing=True)
+        s0.record(stream)
+        for _ in range(args.kernel_reps):
+            fn()
+        s1.record(stream)
+        torch.cuda.synchronize()
+        ms = s0.elapsed_time(s1) / args.kernel_reps
+        kres[name] = {"ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 1) if fl else 0.0,
+                      "gbs": round(ntens * tensor_bytes / (ms * 1e-3) / 1e9, 1)}
+
+    full_ms = sum(per_code.get(0, [])) / max(1, len(per_code.get(0, [])))
+    full_flops = code_flops(0, B, H, L, d, w)
+    achieved = full_flops / (full_ms * 1e-3) / 1e12 if full_ms > 0 else 0.0
+    plan_layer_steps = NL * NS
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "B": B, "H": H, "L": L, "d": d, "w": w, "layers": NL,
+                   "denoise_steps": NS, "refresh_every": cfg.refresh_every, "plan_seed": cfg.plan_seed,
+                   "ocache": "aliased to the layer output (AST is a no-op)"},
+        "ms_per_layer_step": {
+            "plan": round(ms_per_step / plan_layer_steps, 4),
+            "full_only": round(full_only_ms / plan_layer_steps, 4),
+            **{dfa.CODE_NAMES[c].lower(): round(sum(v) / len(v), 4) for c, v in sorted(per_code.items())},
+        },
+        "plan_speedup_vs_full_only": round(full_only_ms / ms_per_step, 3),
+        "plan_code_counts": {dfa.CODE_NAMES[c].lower(): int((code == c).sum()) for c in range(5)},
+        "full_equiv_tflops": round(plan_layer_steps * full_flops / (ms_per_step * 1e-3) / 1e12, 1),
+        "kernels": kres,
+        "reuse_speedup_vs_full": round(kres["full"]["ms"] / kres["wars_reuse"]["ms"], 3),
+        "reuse_ideal_speedup": round(L * L / n_band(L, w), 3),
+        "roofline": {"kernel": "attn_kernel<72, FULL> (dfa_attn_full / FULL plan entries)", "bound": "mfma",
+                     "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "launch_ms": round(full_ms, 4), "flops_per_launch": full_flops},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,155 @@
+/*
+ * dfa.h -- C ABI of the DiTFastAttn attention hot path on AMD MI355X (gfx950).
+ *
+ * DiTFastAttn (arXiv 2406.08552) compresses the self-attention of a diffusion
+ * transformer with three techniques that this library executes on the GPU:
+ *
+ *   WA-RS  Window Attention with Residual Sharing (Sec. 3.2, Eq. 1-2).  At the
+ *          first step r of a residual-sharing set the layer computes full
+ *          attention O_r and window attention W_r and keeps R_r = O_r - W_r;
+ *          at every later step k of the set it computes only W_k and emits
+ *          O_k = W_k + R_r.
+ *   AST    Attention Sharing across Timesteps (Sec. 3.3): a step reuses the
+ *          cached attention output of an earlier step of the same layer.
+ *   ASC    Attention Sharing across CFG (Sec. 3.4): the attention output of
+ *          the conditional evaluation is reused for the unconditional one.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *   Tensors  Q, K, V, O and Ocache are DEVICE pointers to bf16 values
+ *            (16-bit storage, round-to-nearest-even on output); the residual
+ *            R is a DEVICE pointer to fp32 values.  All are contiguous
+ *            [B][H][L][d] with d fastest, and each pointer must be 16-byte
+ *            aligned.  The softmax scale is fixed at 1/sqrt(d).  R is kept in
+ *            fp32 because it is reused unchanged by every later step of its
+ *            set: with a narrow band R is as large as V itself, and bf16
+ *            storage alone would put about 1e-3 mean error into every reuse.
+ *   Window   Window attention attends, for query token i, to the keys j with
+ *            |i - j| <= w over the flattened token index (a band along the
+ *            diagonal of the attention matrix, Sec. 3.2), truncated at 0 and
+ *            L-1.  w is the HALF-width; w >= L-1 covers every key.
+ *   CFG      A classifier-free-guidance batch holds B = 2P entries: entries
+ *            0..P-1 are the conditional evaluations and entry b + P is the
+ *            unconditional partner of entry b (Sec. 3.4).
+ *   Sizes    B, H, L >= 1; w >= 0; d in {64, 72} (others return
+ *            DFA_ERR_UNSUPPORTED).  L is arbitrary: ragged tiles are masked.
+ *   Streams  Every call is asynchronous on `stream` (0 = the null stream).
+ *            Outputs are valid once the caller has synchronised the stream.
+ *   Memory   The caller allocates and owns every buffer and the stream.  The
+ *            library never allocates, frees or synchronises, keeps no pointer
+ *            after returning and holds no state between calls: calls are
+ *            re-entrant and calls on different streams may run concurrently
+ *            as long as their output buffers do not overlap.
+ *   Errors   Every function returns a dfa_status; nothing else crosses the
+ *            ABI.  Arguments are validated before any HIP call is made, so a
+ *            bad argument is reported without touching a device.  After a
+ *            non-OK status dfa_last_error() describes it.
+ */
+#ifndef DFA_H
+#define DFA_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DFA_OK = 0,
+    DFA_ERR_INVALID_ARG = 1,  /* NULL/misaligned pointer, bad size, bad code, aliasing */
+    DFA_ERR_UNSUPPORTED = 2,  /* valid but not built (head dim outside the supported set) */
+    DFA_ERR_HIP = 3           /* a HIP launch or query failed; see dfa_last_error() */
+} dfa_status;
+
+/* Plan codes: the strategy one layer runs at one denoising step (the entries
+ * of the per-(step, layer) plan dictionary produced by the plan search of
+ * Sec. 3.5, Alg. 1). */
+enum {
+    DFA_FULL = 0,          /* full attention                                  */
+    DFA_WARS_REFRESH = 1,  /* WA-RS, first step of a set: O = Attn, R = O - W  (Eq. 1) */
+    DFA_WARS_REUSE = 2,    /* WA-RS, later step:          O = W + R            (Eq. 2) */
+    DFA_AST_REUSE = 3,     /* AST: O = the layer's cached output (Sec. 3.3)    */
+    DFA_ASC_REUSE = 4      /* ASC: conditional half computed, copied to the unconditional half (Sec. 3.4) */
+};
+
+/* Full self-attention (Sec. 3.2, first line of Eq. 1):
+ *   O[b,h,i,:] = sum_j softmax_j(Q[b,h,i,:] . K[b,h,j,:] / sqrt(d)) V[b,h,j,:]
+ * In:  Q, K, V.  Out: O (must not overlap Q, K or V).
+ * R and w are accepted for signature symmetry with the other calls and are
+ * ignored (R may be NULL; w must still be >= 0). */
+dfa_status dfa_attn_full(const void* Q, const void* K, const void* V, void* O, void* R,
+                         int B, int H, int L, int d, int w, hipStream_t stream);
+
+/* WA-RS refresh (Sec. 3.2, Eq. 1) in one pass over K and V:
+ *   O := Attention(Q, K, V)                       (full attention, O_r)
+ *   R := O_full - WindowAttention(Q, K, V; w)     (the residual R_r)
+ * Both outputs are computed from the same scores; R (fp32) is the difference
+ * of the two fp32 results.  O and R must not overlap each other or Q, K, V.
+ * w >= L-1 gives R == 0 exactly. */
+dfa_status dfa_attn_full_and_residual(const void* Q, const void* K, const void* V, void* O, void* R,
+                                      int B, int H, int L, int d, int w, hipStream_t stream);
+
+/* WA-RS reuse (Sec. 3.2, Eq. 2):
+ *   O := WindowAttention(Q, K, V; w) + R
+ * Only key tiles that intersect the band are visited.  R is the residual of
+ * the layer's latest refresh; R == NULL gives plain window attention.  O must
+ * not overlap Q, K, V or R. */
+dfa_status dfa_attn_window_plus_residual(const void* Q, const void* K, const void* V, void* O,
+                                         const void* R, int B, int H, int L, int d, int w,
+                                         hipStream_t stream);
+
+/* One plan entry of one layer at one step: dispatches `code` and maintains the
+ * caller's per-layer caches.
+ *   R       the layer's fp32 residual buffer [B,H,L,d]: written by DFA_WARS_REFRESH,
+ *           read by DFA_WARS_REUSE (required for both; ignored otherwise).
+ *   Ocache  the layer's output cache [B,H,L,d] for AST (Sec. 3.3).  Every
+ *           computed step (all codes except AST) also writes its output here,
+ *           and DFA_AST_REUSE copies it to O.  Ocache == O makes AST a no-op
+ *           and computed steps write once.  Ocache == NULL is allowed for
+ *           every code except DFA_AST_REUSE.
+ *   code    FULL      O = Attention
+ *           REFRESH   O = Attention, R = O - W
+ *           REUSE     O = W + R
+ *           AST       O = Ocache
+ *           ASC       O[b] = O[b+B/2] = Attention on the conditional entry b
+ *                     (b < B/2; B must be even)
+ * The ASC copy and the cache write are fused into the attention kernel's
+ * store (each output tile is written to every destination), not separate
+ * passes.  Returns DFA_ERR_INVALID_ARG for an unknown code, odd B with ASC,
+ * a missing R or Ocache, or overlapping outputs. */
+dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, void* O, void* R,
+                         void* Ocache, int B, int H, int L, int d, int w, hipStream_t stream);
+
+/* Host only (no device is touched).  Draws a seeded per-(step, layer) plan in
+ * place of the searched plan dictionary of Alg. 1 and resolves its cache
+ * sources.  Output arrays are int32, step-major [n_steps][n_layers]:
+ *   code[t][l]   executed plan code (DFA_FULL .. DFA_ASC_REUSE)
+ *   r_src[t][l]  for DFA_WARS_REUSE the step whose residual is read, else -1
+ *   o_src[t][l]  for DFA_AST_REUSE the step whose output is returned, else t
+ * Drawing: a SplitMix64 stream (Steele, Lea and Flood 2014) seeded with
+ * `seed`, one draw per entry in step-major order; the draw's upper 32 bits
+ * map to a code by ((x >> 32) * 5) >> 32.  Legality repair, in order:
+ *   1. AST before the layer has a cached output             -> FULL
+ *   2. refresh_every > 0: REFRESH and REUSE draws both mean WA-RS; the entry
+ *      is REFRESH when the layer has no residual or its residual is at least
+ *      refresh_every steps old, else REUSE
+ *   3. refresh_every == 0: REUSE before the layer's first refresh -> REFRESH
+ *   4. ASC drawn with an odd B                             -> DFA_ERR_INVALID_ARG
+ * n_layers, n_steps, B >= 1 and refresh_every >= 0 are required. */
+dfa_status dfa_plan_make(uint64_t seed, int n_layers, int n_steps, int refresh_every, int B,
+                         int32_t* code, int32_t* r_src, int32_t* o_src);
+
+/* Message for the last non-OK status returned on the calling thread (an empty
+ * string if there was none).  The pointer stays valid until the next call on
+ * the same thread. */
+const char* dfa_last_error(void);
+
+/* Library version as "major.minor.patch". */
+const char* dfa_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DFA_H */

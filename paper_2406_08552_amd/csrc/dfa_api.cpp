@@ -1,0 +1,302 @@
+// Host side of the C ABI declared in include/dfa.h: argument validation,
+// dispatch of the plan codes to the HIP kernels, the seeded plan generator
+// and the per-thread error message.
+//
+// Validation always runs before the first HIP call, so every argument error
+// is reported on a machine without a GPU.
+#include "dfa.h"
+
+#include <stdarg.h>
+#include <stdint.h>
+#include <stdio.h>
+
+#include <string>
+#include <vector>
+
+#include "dfa_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dfa_status fail(dfa_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+dfa_status hip_status(hipError_t e, const char* what) {
+    if (e == hipSuccess) return DFA_OK;
+    return fail(DFA_ERR_HIP, "%s: %s (%s)", what, hipGetErrorName(e), hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// [a, a + na) and [b, b + nb) intersect
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    return x < y + nb && y < x + na;
+}
+
+bool overlaps(const void* a, const void* b, size_t n) { return overlaps(a, n, b, n); }
+
+struct Shape {
+    int B, H, L, d, w;
+    size_t bytes;    // one [B,H,L,d] bf16 tensor
+    size_t rbytes;   // the fp32 residual [B,H,L,d]
+};
+
+dfa_status check_shape(int B, int H, int L, int d, int w, Shape* s) {
+    if (B <= 0 || H <= 0 || L <= 0 || d <= 0)
+        return fail(DFA_ERR_INVALID_ARG, "sizes must be positive (B=%d H=%d L=%d d=%d)", B, H, L, d);
+    if (w < 0) return fail(DFA_ERR_INVALID_ARG, "window half-width w=%d must be >= 0", w);
+    const unsigned long long elems = (unsigned long long)B * H * L * d;
+    if (elems > (1ULL << 40)) return fail(DFA_ERR_INVALID_ARG, "tensor of %llu elements is too large", elems);
+    if ((unsigned long long)B * H > (1ULL << 24)) return fail(DFA_ERR_INVALID_ARG, "B*H=%lld is too large", (long long)B * H);
+    if (!dfa::head_dim_supported(d)) return fail(DFA_ERR_UNSUPPORTED, "head dim d=%d is not built (supported: 64, 72)", d);
+    s->B = B;
+    s->H = H;
+    s->L = L;
+    s->d = d;
+    s->w = w;
+    s->bytes = (size_t)elems * 2;
+    s->rbytes = (size_t)elems * 4;
+    return DFA_OK;
+}
+
+dfa_status check_ptr(const void* p, const char* name) {
+    if (!p) return fail(DFA_ERR_INVALID_ARG, "%s is NULL", name);
+    if (!aligned16(p)) return fail(DFA_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+    return DFA_OK;
+}
+
+dfa_status check_qkv(const void* Q, const void* K, const void* V) {
+    dfa_status st;
+    if ((st = check_ptr(Q, "Q")) != DFA_OK) return st;
+    if ((st = check_ptr(K, "K")) != DFA_OK) return st;
+    return check_ptr(V, "V");
+}
+
+// an output buffer of out_bytes must not overlap any input tensor of in_bytes
+dfa_status check_out_vs_inputs(const void* out, const char* name, const void* Q, const void* K, const void* V,
+                               size_t in_bytes, size_t out_bytes) {
+    if (overlaps(out, out_bytes, Q, in_bytes) || overlaps(out, out_bytes, K, in_bytes) ||
+        overlaps(out, out_bytes, V, in_bytes))
+        return fail(DFA_ERR_INVALID_ARG, "%s overlaps Q, K or V", name);
+    return DFA_OK;
+}
+
+dfa_status check_out_vs_inputs(const void* out, const char* name, const void* Q, const void* K, const void* V,
+                               size_t bytes) {
+    return check_out_vs_inputs(out, name, Q, K, V, bytes, bytes);
+}
+
+dfa::AttnLaunch make_launch(const void* Q, const void* K, const void* V, const Shape& s) {
+    dfa::AttnLaunch a{};
+    a.Q = Q;
+    a.K = K;
+    a.V = V;
+    a.B = s.B;
+    a.H = s.H;
+    a.L = s.L;
+    a.d = s.d;
+    a.w = s.w;
+    return a;
+}
+
+// The output cache is written by computed steps unless it is O itself.
+bool cache_is_separate(const void* O, const void* Oc) { return Oc != nullptr && Oc != O; }
+
+dfa_status check_cache(const void* O, const void* Oc, const void* Q, const void* K, const void* V, const void* R,
+                       size_t bytes, size_t rbytes) {
+    if (!cache_is_separate(O, Oc)) return DFA_OK;
+    dfa_status st;
+    if ((st = check_ptr(Oc, "Ocache")) != DFA_OK) return st;
+    if ((st = check_out_vs_inputs(Oc, "Ocache", Q, K, V, bytes)) != DFA_OK) return st;
+    if (overlaps(Oc, O, bytes)) return fail(DFA_ERR_INVALID_ARG, "Ocache partially overlaps O");
+    if (R && overlaps(Oc, bytes, R, rbytes)) return fail(DFA_ERR_INVALID_ARG, "Ocache overlaps R");
+    return DFA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dfa_last_error(void) { return g_last_error.c_str(); }
+
+const char* dfa_version(void) { return "0.1.0"; }
+
+dfa_status dfa_attn_full(const void* Q, const void* K, const void* V, void* O, void* R, int B, int H, int L, int d,
+                         int w, hipStream_t stream) {
+    (void)R;
+    Shape s;
+    dfa_status st;
+    if ((st = check_shape(B, H, L, d, w, &s)) != DFA_OK) return st;
+    if ((st = check_qkv(Q, K, V)) != DFA_OK) return st;
+    if ((st = check_ptr(O, "O")) != DFA_OK) return st;
+    if ((st = check_out_vs_inputs(O, "O", Q, K, V, s.bytes)) != DFA_OK) return st;
+    dfa::AttnLaunch a = make_launch(Q, K, V, s);
+    a.dst[0] = O;
+    a.ndst = 1;
+    return hip_status(dfa::launch_full(a, stream), "dfa_attn_full launch");
+}
+
+dfa_status dfa_attn_full_and_residual(const void* Q, const void* K, const void* V, void* O, void* R, int B, int H,
+                                      int L, int d, int w, hipStream_t stream) {
+    Shape s;
+    dfa_status st;
+    if ((st = check_shape(B, H, L, d, w, &s)) != DFA_OK) return st;
+    if ((st = check_qkv(Q, K, V)) != DFA_OK) return st;
+    if ((st = check_ptr(O, "O")) != DFA_OK) return st;
+    if ((st = check_ptr(R, "R")) != DFA_OK) return st;
+    if ((st = check_out_vs_inputs(O, "O", Q, K, V, s.bytes)) != DFA_OK) return st;
+    if ((st = check_out_vs_inputs(R, "R", Q, K, V, s.bytes, s.rbytes)) != DFA_OK) return st;
+    if (overlaps(O, s.bytes, R, s.rbytes)) return fail(DFA_ERR_INVALID_ARG, "O and R overlap");
+    dfa::AttnLaunch a = make_launch(Q, K, V, s);
+    a.dst[0] = O;
+    a.ndst = 1;
+    a.Rout = R;
+    return hip_status(dfa::launch_refresh(a, stream), "dfa_attn_full_and_residual launch");
+}
+
+dfa_status dfa_attn_window_plus_residual(const void* Q, const void* K, const void* V, void* O, const void* R, int B,
+                                         int H, int L, int d, int w, hipStream_t stream) {
+    Shape s;
+    dfa_status st;
+    if ((st = check_shape(B, H, L, d, w, &s)) != DFA_OK) return st;
+    if ((st = check_qkv(Q, K, V)) != DFA_OK) return st;
+    if ((st = check_ptr(O, "O")) != DFA_OK) return st;
+    if (R && !aligned16(R)) return fail(DFA_ERR_INVALID_ARG, "R is not 16-byte aligned");
+    if ((st = check_out_vs_inputs(O, "O", Q, K, V, s.bytes)) != DFA_OK) return st;
+    if (R && overlaps(O, s.bytes, R, s.rbytes)) return fail(DFA_ERR_INVALID_ARG, "O and R overlap");
+    dfa::AttnLaunch a = make_launch(Q, K, V, s);
+    a.dst[0] = O;
+    a.ndst = 1;
+    a.Rin = R;
+    return hip_status(dfa::launch_window(a, stream), "dfa_attn_window_plus_residual launch");
+}
+
+dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, void* O, void* R, void* Ocache,
+                         int B, int H, int L, int d, int w, hipStream_t stream) {
+    if (code < DFA_FULL || code > DFA_ASC_REUSE) return fail(DFA_ERR_INVALID_ARG, "unknown plan code %d", code);
+    Shape s;
+    dfa_status st;
+    if ((st = check_shape(B, H, L, d, w, &s)) != DFA_OK) return st;
+    if ((st = check_ptr(O, "O")) != DFA_OK) return st;
+    const bool sep = cache_is_separate(O, Ocache);
+
+    if (code == DFA_AST_REUSE) {
+        // no attention: Q/K/V are not read and may be NULL
+        if (!Ocache) return fail(DFA_ERR_INVALID_ARG, "AST needs the layer's output cache (Ocache is NULL)");
+        if (!sep) return DFA_OK;  // the output already lives in the cache
+        if ((st = check_ptr(Ocache, "Ocache")) != DFA_OK) return st;
+        if (overlaps(O, Ocache, s.bytes)) return fail(DFA_ERR_INVALID_ARG, "Ocache partially overlaps O");
+        return hip_status(dfa::launch_copy(Ocache, O, s.bytes, stream), "AST copy launch");
+    }
+
+    if ((st = check_qkv(Q, K, V)) != DFA_OK) return st;
+    if ((st = check_out_vs_inputs(O, "O", Q, K, V, s.bytes)) != DFA_OK) return st;
+    const bool uses_r = code == DFA_WARS_REFRESH || code == DFA_WARS_REUSE;
+    if (uses_r) {
+        if ((st = check_ptr(R, "R")) != DFA_OK) return st;
+        if ((st = check_out_vs_inputs(R, "R", Q, K, V, s.bytes, s.rbytes)) != DFA_OK) return st;
+        if (overlaps(O, s.bytes, R, s.rbytes)) return fail(DFA_ERR_INVALID_ARG, "O and R overlap");
+    }
+    if ((st = check_cache(O, Ocache, Q, K, V, uses_r ? R : nullptr, s.bytes, s.rbytes)) != DFA_OK) return st;
+
+    dfa::AttnLaunch a = make_launch(Q, K, V, s);
+    a.dst[0] = O;
+    a.ndst = 1;
+    if (code == DFA_ASC_REUSE) {
+        if (B % 2) return fail(DFA_ERR_INVALID_ARG, "ASC needs an even batch (B=%d)", B);
+        // attention on the conditional half; every output tile is also stored
+        // at its unconditional partner (and in the cache)
+        const size_t half = s.bytes / 2;
+        a.B = B / 2;
+        a.dst[a.ndst++] = (char*)O + half;
+        if (sep) {
+            a.dst[a.ndst++] = Ocache;
+            a.dst[a.ndst++] = (char*)Ocache + half;
+        }
+        return hip_status(dfa::launch_full(a, stream), "ASC launch");
+    }
+    if (sep) a.dst[a.ndst++] = Ocache;
+    switch (code) {
+        case DFA_FULL:
+            return hip_status(dfa::launch_full(a, stream), "FULL launch");
+        case DFA_WARS_REFRESH:
+            a.Rout = R;
+            return hip_status(dfa::launch_refresh(a, stream), "WA-RS refresh launch");
+        default:  // DFA_WARS_REUSE
+            a.Rin = R;
+            return hip_status(dfa::launch_window(a, stream), "WA-RS reuse launch");
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Seeded plan generator
+// ---------------------------------------------------------------------------
+namespace {
+
+// SplitMix64 (Steele, Lea and Flood, "Fast splittable pseudorandom number
+// generators", OOPSLA 2014): a Weyl sequence with the golden-ratio increment
+// followed by two xor-shift-multiply rounds.
+struct SplitMix64 {
+    uint64_t x;
+    uint64_t next() {
+        x += 0x9E3779B97F4A7C15ULL;
+        uint64_t z = x;
+        z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+        z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+        return z ^ (z >> 31);
+    }
+};
+
+}  // namespace
+
+dfa_status dfa_plan_make(uint64_t seed, int n_layers, int n_steps, int refresh_every, int B, int32_t* code,
+                         int32_t* r_src, int32_t* o_src) {
+    if (n_layers <= 0 || n_steps <= 0 || B <= 0 || refresh_every < 0)
+        return fail(DFA_ERR_INVALID_ARG, "bad plan dimensions (layers=%d steps=%d refresh_every=%d B=%d)", n_layers,
+                    n_steps, refresh_every, B);
+    if ((long long)n_layers * n_steps > (1LL << 30)) return fail(DFA_ERR_INVALID_ARG, "plan too large");
+    if (!code || !r_src || !o_src) return fail(DFA_ERR_INVALID_ARG, "plan output arrays must not be NULL");
+
+    SplitMix64 rng{seed};
+    std::vector<int> last_refresh(n_layers, -1);  // step of the layer's latest REFRESH
+    std::vector<int> cached(n_layers, -1);        // step whose output the layer's cache holds
+    for (int t = 0; t < n_steps; ++t) {
+        for (int l = 0; l < n_layers; ++l) {
+            const uint64_t hi = rng.next() >> 32;
+            int c = (int)((hi * 5u) >> 32);
+            if (c == DFA_AST_REUSE && cached[l] < 0) c = DFA_FULL;
+            if (c == DFA_WARS_REFRESH || c == DFA_WARS_REUSE) {
+                if (refresh_every > 0) {
+                    const bool stale = last_refresh[l] < 0 || t - last_refresh[l] >= refresh_every;
+                    c = stale ? DFA_WARS_REFRESH : DFA_WARS_REUSE;
+                } else if (c == DFA_WARS_REUSE && last_refresh[l] < 0) {
+                    c = DFA_WARS_REFRESH;
+                }
+            }
+            if (c == DFA_ASC_REUSE && (B & 1))
+                return fail(DFA_ERR_INVALID_ARG, "ASC drawn at step %d layer %d with odd B=%d", t, l, B);
+            const size_t e = (size_t)t * n_layers + l;
+            code[e] = c;
+            r_src[e] = (c == DFA_WARS_REUSE) ? last_refresh[l] : -1;
+            if (c == DFA_AST_REUSE) {
+                o_src[e] = cached[l];
+            } else {
+                o_src[e] = t;
+                cached[l] = t;
+            }
+            if (c == DFA_WARS_REFRESH) last_refresh[l] = t;
+        }
+    }
+    return DFA_OK;
+}
+
+}  // extern "C"

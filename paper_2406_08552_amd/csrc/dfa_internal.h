@@ -1,0 +1,32 @@
+// Internal interface between the host library (argument checks, dispatch,
+// plan generator) and the HIP kernels.  Not part of the public ABI.
+#ifndef DFA_INTERNAL_H
+#define DFA_INTERNAL_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+namespace dfa {
+
+// One attention launch over B batch entries.  Every destination in dst[]
+// receives the same output at the same element offset.
+struct AttnLaunch {
+    const void* Q;
+    const void* K;
+    const void* V;
+    const void* Rin;   // window kernel: fp32 residual added to the output (may be null)
+    void* Rout;        // refresh kernel: fp32 residual output
+    void* dst[4];
+    int ndst;
+    int B, H, L, d, w;
+};
+
+bool head_dim_supported(int d);
+hipError_t launch_full(const AttnLaunch& a, hipStream_t stream);
+hipError_t launch_refresh(const AttnLaunch& a, hipStream_t stream);
+hipError_t launch_window(const AttnLaunch& a, hipStream_t stream);
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
+
+}  // namespace dfa
+
+#endif

@@ -1,0 +1,590 @@
+// Attention kernels of the DiTFastAttn hot path for gfx950 (CDNA4).
+//
+// One kernel template covers the three attention operations of the method:
+//   MODE_FULL     O = softmax(Q K^T / sqrt(d)) V                 (Sec. 3.2, Eq. 1 first line)
+//   MODE_REFRESH  O = full attention, R = O - window attention    (Sec. 3.2, Eq. 1), R in fp32
+//   MODE_WINDOW   O = window attention (+ R when given)           (Sec. 3.2, Eq. 2)
+// The window is the band |i - j| <= w over the flattened token index.
+//
+// Work decomposition
+//   A workgroup is 4 wavefronts and owns BQ = 128 consecutive queries of one
+//   (batch, head); each wavefront owns 32 of them (two 16-query MFMA blocks).
+//   The workgroup walks key tiles of BK = 64 keys, staged in LDS with double
+//   buffering (global loads of tile t+1 are in flight while tile t is used).
+//
+// MFMA mapping (v_mfma_f32_16x16x32_bf16, fp32 accumulation)
+//   Scores are formed transposed, S^T = K Q^T: A = 16 keys x 32 dims from LDS,
+//   B = 32 dims x 16 queries held in registers for the whole kernel.  The
+//   result leaves every lane with a single query (lane % 16) and four keys
+//   per 16-key block, so softmax statistics are per-lane values reduced over
+//   the four lane groups only.  The same registers, rounded to bf16, are
+//   directly the B operand of the second product O^T = V^T P^T, whose A
+//   operand is read from a transposed copy of the V tile in LDS.  The output
+//   accumulator keeps the same one-query-per-lane layout, so the online
+//   softmax rescale needs no data movement.
+//   Head dim 72 = 2 x 32 + 8: the last 8 dims go through one 16x16x16 MFMA
+//   (k padded to 16); PV pads the 72 output dims to 5 blocks of 16.  The
+//   padding row 72 of V^T is set to 1.0, so the PV product also yields the
+//   softmax row sum (the sum of the same bf16 probabilities that weight V).
+//
+// Online softmax
+//   Per query a running max m (log2 domain) and accumulator (O, l).  The max
+//   is updated lazily: the accumulator is rescaled only when a tile's max
+//   exceeds m by more than 8 (so probabilities stay below 2^8 and the
+//   rescale is almost never taken after the first tiles).
+//
+// Band handling
+//   Each wavefront classifies every key tile against its 32 queries: fully
+//   inside the band, fully outside, or straddling it (element mask).  The
+//   window kernel visits only the tiles that intersect the workgroup's band
+//   and skips per wavefront the ones outside it; the refresh kernel sends
+//   inside tiles to the in-band accumulator, outside tiles to the out-of-band
+//   accumulator and splits straddling tiles by element, so every score
+//   feeds exactly one accumulator and K/V are streamed once.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dfa_internal.h"
+
+namespace dfa {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int NWAVES = 4;
+constexpr int NTHREADS = NWAVES * 64;
+constexpr int BK = 64;                    // keys per tile
+constexpr int NKB = BK / 16;              // 16-key blocks per tile
+constexpr int QBW = 2;                    // 16-query blocks per wavefront
+constexpr int BQ = NWAVES * QBW * 16;     // queries per workgroup
+constexpr float RESCALE_THRESH = 8.0f;    // lazy rescale margin (log2 units)
+constexpr float NEG_INF = -__builtin_inff();
+
+enum { MODE_FULL = 0, MODE_REFRESH = 1, MODE_WINDOW = 2 };
+enum { MASK_NONE = 0, MASK_KEYS = 1, MASK_BAND_IN = 2, MASK_BAND_OUT = 3 };
+enum { TILE_INSIDE = 0, TILE_OUTSIDE = 1, TILE_BOUNDARY = 2 };
+
+// Geometry derived from the head dim.
+template <int D>
+struct Geo {
+    static_assert(D % 8 == 0 && D <= 128, "head dim must be a multiple of 8, at most 128");
+    static_assert(D % 32 == 0 || D % 32 == 8 || D % 32 == 16, "unsupported head dim remainder");
+    static constexpr int NC32 = D / 32;              // k=32 chunks of the score product
+    static constexpr int D32 = NC32 * 32;
+    static constexpr int TAIL = D - D32;             // dims left for one k=16 chunk (0, 8, 16)
+    static constexpr int NDB = (D + 15) / 16;        // 16-dim output blocks of PV
+    static constexpr int DPV = NDB * 16;             // padded output dims
+    static constexpr bool ONES = (D % 16) != 0;      // a padding row of V^T carries ones
+    static constexpr int NCH = D / 8;                // 16-byte chunks per row
+    // K row pitch in LDS (elements): a 16-byte read by 16 consecutive rows hits
+    // 16 distinct 4-bank groups when the pitch in dwords is 4 mod 32.
+    static constexpr int KREAD = (TAIL > 8) ? D32 + 16 : D;
+    static constexpr int KP = ((KREAD / 2 + 27) / 32) * 64 + 8;
+    static constexpr int VP = BK + 4;                // V^T row pitch: dwords 2 mod 32
+    static constexpr int KS_ELEMS = BK * KP;
+    static constexpr int VS_ELEMS = DPV * VP;
+    static constexpr int STAGE_ELEMS = KS_ELEMS + VS_ELEMS;
+    static constexpr int KLOADS = (BK * NCH + NTHREADS - 1) / NTHREADS;
+    static constexpr int VITEMS = (BK / 4) * NCH;    // (4-key group, chunk) work items
+    static_assert(VITEMS <= NTHREADS, "V tile needs more than one item per thread");
+    static_assert((KP / 2) % 32 == 4 && KP >= KREAD, "K pitch");
+};
+
+struct Params {
+    const uint16_t* Q;
+    const uint16_t* K;
+    const uint16_t* V;
+    const float* Rin;         // MODE_WINDOW: fp32 residual added to the output (or null)
+    float* Rout;              // MODE_REFRESH: fp32 residual output
+    uint16_t* dst[4];         // every destination receives the same output tile
+    int ndst;
+    int H, L, w;
+    int n_qt;                 // query tiles per (batch, head)
+    int nblocks;
+    float c;                  // log2(e) / sqrt(d)
+};
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ bf16x4 as_bf16x4(u32x2 v) { return __builtin_bit_cast(bf16x4, v); }
+
+// fp32 -> bf16 with round-to-nearest-even (finite inputs, and +-inf).
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+    return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
+}
+
+__device__ __forceinline__ float wave_max_groups(float x) {
+    // reduce over the four 16-lane groups that share a query column
+    x = fmaxf(x, __shfl_xor(x, 16));
+    x = fmaxf(x, __shfl_xor(x, 32));
+    return x;
+}
+
+__device__ __forceinline__ float wave_sum_groups(float x) {
+    x += __shfl_xor(x, 16);
+    x += __shfl_xor(x, 32);
+    return x;
+}
+
+// One score tile, passed by value where a masked private copy is needed.
+struct Tile {
+    f32x4 s[QBW][NKB];
+};
+
+template <int D>
+struct Acc {
+    f32x4 o[QBW][Geo<D>::NDB];   // O^T: lane holds dims 16*m + 4*g + i of query lane%16
+    float m[QBW];                // running max, log2 domain (NEG_INF = none yet)
+    float l[QBW];                // lane-partial row sum (unused when a ones row is present)
+
+    __device__ __forceinline__ void init() {
+#pragma unroll
+        for (int qb = 0; qb < QBW; ++qb) {
+#pragma unroll
+            for (int mb = 0; mb < Geo<D>::NDB; ++mb) o[qb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            m[qb] = NEG_INF;
+            l[qb] = 0.f;
+        }
+    }
+};
+
+// Score tile S^T for the wavefront's 32 queries against the 64 keys of one LDS
+// stage: S[qb][kb][i] is the score of query (16*qb + lane%16) and key
+// (16*kb + 4*(lane/16) + i) of the tile.
+template <int D>
+__device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, const bf16x8 (&qa)[QBW][Geo<D>::NC32 > 0 ? Geo<D>::NC32 : 1],
+                                           const bf16x4 (&qt)[QBW], Tile& S, int r, int g) {
+    using G = Geo<D>;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+        const uint16_t* krow = Ks + (16 * kb + r) * G::KP;
+        bf16x8 ka[G::NC32 > 0 ? G::NC32 : 1];
+#pragma unroll
+        for (int c = 0; c < G::NC32; ++c) ka[c] = as_bf16x8(*(const u32x4*)(krow + 32 * c + 8 * g));
+        bf16x4 kt = as_bf16x4(u32x2{0u, 0u});
+        if constexpr (G::TAIL > 0) {
+            if (4 * g < G::TAIL) kt = as_bf16x4(*(const u32x2*)(krow + G::D32 + 4 * g));
+        }
+#pragma unroll
+        for (int qb = 0; qb < QBW; ++qb) {
+            f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < G::NC32; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[c], qa[qb][c], s, 0, 0, 0);
+            if constexpr (G::TAIL > 0) s = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
+                __builtin_bit_cast(__attribute__((ext_vector_type(4))) short, kt),
+                __builtin_bit_cast(__attribute__((ext_vector_type(4))) short, qt[qb]), s, 0, 0, 0);
+            S.s[qb][kb] = s;
+        }
+    }
+}
+
+// Online-softmax update of one accumulator with one score tile, then PV.
+// S is taken by value: the mask is applied to a private copy.
+template <int D, int MASK>
+__device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* __restrict__ Vt,
+                                           int r, int g, int qrow0, int k0, int L, int w, float c) {
+    using G = Geo<D>;
+    // masking
+    if constexpr (MASK != MASK_NONE) {
+#pragma unroll
+        for (int qb = 0; qb < QBW; ++qb) {
+            const int qi = qrow0 + 16 * qb + r;
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int j = k0 + 16 * kb + 4 * g + i;
+                    bool ok = j < L;
+                    if constexpr (MASK == MASK_BAND_IN || MASK == MASK_BAND_OUT) {
+                        const int dist = qi > j ? qi - j : j - qi;
+                        ok = ok && ((MASK == MASK_BAND_IN) ? (dist <= w) : (dist > w));
+                    }
+                    S.s[qb][kb][i] = ok ? S.s[qb][kb][i] : NEG_INF;
+                }
+            }
+        }
+    }
+    // probabilities, packed to bf16 as the B operand of PV
+    bf16x8 pb[QBW][BK / 32];
+#pragma unroll
+    for (int qb = 0; qb < QBW; ++qb) {
+        float mx = NEG_INF;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, S.s[qb][kb][i]);
+        mx = wave_max_groups(mx) * c;
+        const bool need = mx > acc.m[qb] + RESCALE_THRESH;
+        if (__any(need)) {
+            const float mnew = need ? mx : acc.m[qb];
+            const float alpha = need ? __builtin_amdgcn_exp2f(acc.m[qb] - mnew) : 1.0f;
+#pragma unroll
+            for (int mb = 0; mb < G::NDB; ++mb) acc.o[qb][mb] *= alpha;
+            acc.l[qb] *= alpha;
+            acc.m[qb] = mnew;
+        }
+        const float mbase = acc.m[qb] == NEG_INF ? 0.0f : acc.m[qb];
+        float psum = 0.f;
+#pragma unroll
+        for (int h = 0; h < BK / 32; ++h) {
+            uint32_t wds[4];
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const f32x4 s = S.s[qb][2 * h + half];
+                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0], c, -mbase));
+                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1], c, -mbase));
+                const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2], c, -mbase));
+                const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[3], c, -mbase));
+                if constexpr (!G::ONES) psum += (p0 + p1) + (p2 + p3);
+                wds[2 * half + 0] = f32_to_bf16_bits(p0) | (f32_to_bf16_bits(p1) << 16);
+                wds[2 * half + 1] = f32_to_bf16_bits(p2) | (f32_to_bf16_bits(p3) << 16);
+            }
+            pb[qb][h] = as_bf16x8(u32x4{wds[0], wds[1], wds[2], wds[3]});
+        }
+        if constexpr (!G::ONES) acc.l[qb] += psum;
+    }
+    // O^T += V^T P^T
+#pragma unroll
+    for (int h = 0; h < BK / 32; ++h) {
+#pragma unroll
+        for (int mb = 0; mb < G::NDB; ++mb) {
+            const uint16_t* vrow = Vt + (16 * mb + r) * G::VP + 32 * h + 4 * g;
+            const u32x2 v0 = *(const u32x2*)(vrow);
+            const u32x2 v1 = *(const u32x2*)(vrow + 16);
+            const bf16x8 va = as_bf16x8(u32x4{v0[0], v0[1], v1[0], v1[1]});
+#pragma unroll
+            for (int qb = 0; qb < QBW; ++qb)
+                acc.o[qb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[qb][h], acc.o[qb][mb], 0, 0, 0);
+        }
+    }
+}
+
+// Row sum of one query block, broadcast to every lane of that query.
+template <int D>
+__device__ __forceinline__ float row_sum(const Acc<D>& acc, int qb, int r) {
+    using G = Geo<D>;
+    if constexpr (G::ONES) {
+        constexpr int MB = D / 16, GS = (D % 16) / 4, IS = (D % 16) % 4;
+        return __shfl(acc.o[qb][MB][IS], r + 16 * GS);
+    } else {
+        return wave_sum_groups(acc.l[qb]);
+    }
+}
+
+// Global -> register prefetch of one K/V tile, and register -> LDS store.
+template <int D>
+struct TileLoader {
+    using G = Geo<D>;
+    u32x4 kreg[G::KLOADS];
+    u32x4 vreg[4];
+
+    __device__ __forceinline__ void load(const uint16_t* __restrict__ Kbh, const uint16_t* __restrict__ Vbh, int k0, int L,
+                                         int tid) {
+#pragma unroll
+        for (int it = 0; it < G::KLOADS; ++it) {
+            const int cidx = tid + it * NTHREADS;
+            const int row = cidx / G::NCH, ch = cidx % G::NCH;
+            kreg[it] = u32x4{0u, 0u, 0u, 0u};
+            if (cidx < BK * G::NCH && k0 + row < L)
+                kreg[it] = *(const u32x4*)(Kbh + (size_t)(k0 + row) * D + ch * 8);
+        }
+        if (tid < G::VITEMS) {
+            const int kg = tid / G::NCH, ch = tid % G::NCH;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int row = 4 * kg + e;
+                vreg[e] = u32x4{0u, 0u, 0u, 0u};
+                if (k0 + row < L) vreg[e] = *(const u32x4*)(Vbh + (size_t)(k0 + row) * D + ch * 8);
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store(uint16_t* __restrict__ Ks, uint16_t* __restrict__ Vt, int tid) const {
+#pragma unroll
+        for (int it = 0; it < G::KLOADS; ++it) {
+            const int cidx = tid + it * NTHREADS;
+            const int row = cidx / G::NCH, ch = cidx % G::NCH;
+            if (cidx < BK * G::NCH) *(u32x4*)(Ks + row * G::KP + ch * 8) = kreg[it];
+        }
+        if (tid < G::VITEMS) {
+            const int kg = tid / G::NCH, ch = tid % G::NCH;
+            // transpose 4 keys x 8 dims into 8 rows (dims) x 4 keys
+#pragma unroll
+            for (int cc = 0; cc < 8; ++cc) {
+                const int wi = cc >> 1;
+                uint32_t lo, hi;
+                if (cc & 1) {
+                    lo = (vreg[0][wi] >> 16) | (vreg[1][wi] & 0xFFFF0000u);
+                    hi = (vreg[2][wi] >> 16) | (vreg[3][wi] & 0xFFFF0000u);
+                } else {
+                    lo = (vreg[0][wi] & 0xFFFFu) | (vreg[1][wi] << 16);
+                    hi = (vreg[2][wi] & 0xFFFFu) | (vreg[3][wi] << 16);
+                }
+                *(u32x2*)(Vt + (8 * ch + cc) * G::VP + 4 * kg) = u32x2{lo, hi};
+            }
+        }
+    }
+};
+
+template <int D, int MODE>
+__global__ void __launch_bounds__(NTHREADS) attn_kernel(Params p) {
+    using G = Geo<D>;
+    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int r = lane & 15;
+    const int g = lane >> 4;
+
+    // XCD-aware block order: workgroups are dealt to the 8 XCDs round-robin,
+    // so give each XCD a contiguous range of (head, query-tile) work and the
+    // workgroups sharing an XCD's L2 read the same K/V.
+    int blk = blockIdx.x;
+    if ((p.nblocks & 7) == 0) blk = (blk & 7) * (p.nblocks >> 3) + (blk >> 3);
+    const int bh = blk / p.n_qt;
+    const int qt = blk % p.n_qt;
+    const int L = p.L, w = p.w;
+    const size_t head_off = (size_t)bh * L * D;
+    const uint16_t* __restrict__ Qbh = p.Q + head_off;
+    const uint16_t* __restrict__ Kbh = p.K + head_off;
+    const uint16_t* __restrict__ Vbh = p.V + head_off;
+
+    const int q0 = qt * BQ;                       // workgroup's first query
+    const int qw0 = q0 + wave * (QBW * 16);       // wavefront's first query
+    const int qhi_wg = min(q0 + BQ - 1, L - 1);
+    const int qhi_w = min(qw0 + QBW * 16 - 1, L - 1);
+    const bool wave_active = qw0 < L;
+
+    // key-tile range
+    int t_begin = 0, t_end = (L + BK - 1) / BK;
+    if constexpr (MODE == MODE_WINDOW) {
+        const int klo = max(0, q0 - w);
+        const int khi = (int)min((long long)L - 1, (long long)qhi_wg + w);
+        t_begin = klo / BK;
+        t_end = khi / BK + 1;
+    }
+
+    // constant LDS regions of both stages: V^T padding rows (ones row for the
+    // row sum, zeros otherwise) and the K pitch padding
+    for (int st = 0; st < 2; ++st) {
+        uint16_t* Ks = smem + st * G::STAGE_ELEMS;
+        uint16_t* Vt = Ks + G::KS_ELEMS;
+        for (int idx = tid; idx < (G::DPV - D) * G::VP; idx += NTHREADS) {
+            const int row = D + idx / G::VP;
+            Vt[row * G::VP + idx % G::VP] = (G::ONES && row == D) ? (uint16_t)0x3F80u : (uint16_t)0u;
+        }
+        if constexpr (G::KP > D) {
+            for (int idx = tid; idx < BK * (G::KP - D); idx += NTHREADS)
+                Ks[(idx / (G::KP - D)) * G::KP + D + idx % (G::KP - D)] = 0;
+        }
+    }
+
+    // Q fragments (B operand of S^T = K Q^T), zero beyond L and beyond d
+    bf16x8 qa[QBW][G::NC32 > 0 ? G::NC32 : 1];
+    bf16x4 qt4[QBW];
+#pragma unroll
+    for (int qb = 0; qb < QBW; ++qb) {
+        const int qrow = qw0 + 16 * qb + r;
+        const bool ok = qrow < L;
+        const uint16_t* qp = Qbh + (size_t)(ok ? qrow : 0) * D;
+#pragma unroll
+        for (int c = 0; c < G::NC32; ++c)
+            qa[qb][c] = as_bf16x8(ok ? *(const u32x4*)(qp + 32 * c + 8 * g) : u32x4{0u, 0u, 0u, 0u});
+        qt4[qb] = as_bf16x4(u32x2{0u, 0u});
+        if constexpr (G::TAIL > 0) {
+            if (ok && 4 * g < G::TAIL) qt4[qb] = as_bf16x4(*(const u32x2*)(qp + G::D32 + 4 * g));
+        }
+    }
+
+    Acc<D> acc_in;    // full (MODE_FULL), in-band (REFRESH, WINDOW)
+    Acc<D> acc_out;   // out-of-band (REFRESH only)
+    acc_in.init();
+    if constexpr (MODE == MODE_REFRESH) acc_out.init();
+
+    TileLoader<D> ld;
+    if (t_begin < t_end) {
+        ld.load(Kbh, Vbh, t_begin * BK, L, tid);
+        ld.store(smem, smem + G::KS_ELEMS, tid);
+    }
+    __syncthreads();
+
+    for (int t = t_begin; t < t_end; ++t) {
+        const int stage = (t - t_begin) & 1;
+        const uint16_t* Ks = smem + stage * G::STAGE_ELEMS;
+        const uint16_t* Vt = Ks + G::KS_ELEMS;
+        const bool has_next = t + 1 < t_end;
+        if (has_next) ld.load(Kbh, Vbh, (t + 1) * BK, L, tid);
+
+        const int k0 = t * BK;
+        if (wave_active) {
+            const int khi = min(k0 + BK - 1, L - 1);
+            const bool ragged = k0 + BK > L;
+            int cls = TILE_INSIDE;
+            if constexpr (MODE != MODE_FULL) {
+                const int mind = khi < qw0 ? qw0 - khi : (k0 > qhi_w ? k0 - qhi_w : 0);
+                const int maxd = max(qhi_w - k0, khi - qw0);
+                cls = maxd <= w ? TILE_INSIDE : (mind > w ? TILE_OUTSIDE : TILE_BOUNDARY);
+            }
+            if (MODE != MODE_WINDOW || cls != TILE_OUTSIDE) {
+                Tile S;
+                score_tile<D>(Ks, qa, qt4, S, r, g);
+                if constexpr (MODE == MODE_FULL) {
+                    if (ragged) accumulate<D, MASK_KEYS>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
+                    else accumulate<D, MASK_NONE>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
+                } else if constexpr (MODE == MODE_WINDOW) {
+                    if (cls == TILE_BOUNDARY) accumulate<D, MASK_BAND_IN>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
+                    else if (ragged) accumulate<D, MASK_KEYS>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
+                    else accumulate<D, MASK_NONE>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
+                } else {
+                    if (cls == TILE_BOUNDARY) {
+                        accumulate<D, MASK_BAND_IN>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
+                        accumulate<D, MASK_BAND_OUT>(acc_out, S, Vt, r, g, qw0, k0, L, w, p.c);
+                    } else if (cls == TILE_INSIDE) {
+                        if (ragged) accumulate<D, MASK_KEYS>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
+                        else accumulate<D, MASK_NONE>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
+                    } else {
+                        if (ragged) accumulate<D, MASK_KEYS>(acc_out, S, Vt, r, g, qw0, k0, L, w, p.c);
+                        else accumulate<D, MASK_NONE>(acc_out, S, Vt, r, g, qw0, k0, L, w, p.c);
+                    }
+                }
+            }
+        }
+
+        if (has_next) {
+            uint16_t* Kn = smem + (stage ^ 1) * G::STAGE_ELEMS;
+            ld.store(Kn, Kn + G::KS_ELEMS, tid);
+        }
+        __syncthreads();
+    }
+
+    if (!wave_active) return;
+
+    // epilogue: normalise, combine, store bf16 to every destination
+#pragma unroll
+    for (int qb = 0; qb < QBW; ++qb) {
+        const int qrow = qw0 + 16 * qb + r;
+        const float l_in = row_sum<D>(acc_in, qb, r);
+        float a_in = 1.f, a_out = 0.f, inv_full = 0.f;
+        if constexpr (MODE == MODE_REFRESH) {
+            const float l_out = row_sum<D>(acc_out, qb, r);
+            const float m_in = acc_in.m[qb], m_out = acc_out.m[qb];
+            const float M = fmaxf(m_in, m_out);
+            a_in = (m_in == M) ? 1.f : __builtin_amdgcn_exp2f(m_in - M);
+            a_out = (m_out == NEG_INF) ? 0.f : ((m_out == M) ? 1.f : __builtin_amdgcn_exp2f(m_out - M));
+            inv_full = 1.f / (l_in * a_in + l_out * a_out);
+        }
+        const float inv_in = 1.f / l_in;
+        if (qrow >= L) continue;
+        const size_t row_off = head_off + (size_t)qrow * D;
+#pragma unroll
+        for (int mb = 0; mb < G::NDB; ++mb) {
+            const int col = 16 * mb + 4 * g;
+            if (col >= D) continue;
+            const size_t off = row_off + col;
+            float o[4], res[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float win = acc_in.o[qb][mb][i] * inv_in;
+                if constexpr (MODE == MODE_REFRESH) {
+                    const float full = (acc_in.o[qb][mb][i] * a_in + acc_out.o[qb][mb][i] * a_out) * inv_full;
+                    o[i] = full;
+                    res[i] = full - win;
+                } else {
+                    o[i] = win;
+                }
+            }
+            if constexpr (MODE == MODE_WINDOW) {
+                if (p.Rin) {
+                    const f32x4 rv = *(const f32x4*)(p.Rin + off);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) o[i] += rv[i];
+                }
+            }
+            const u32x2 ov = u32x2{f32_to_bf16_bits(o[0]) | (f32_to_bf16_bits(o[1]) << 16),
+                                   f32_to_bf16_bits(o[2]) | (f32_to_bf16_bits(o[3]) << 16)};
+            for (int di = 0; di < p.ndst; ++di) *(u32x2*)(p.dst[di] + off) = ov;
+            if constexpr (MODE == MODE_REFRESH) {
+                *(f32x4*)(p.Rout + off) = f32x4{res[0], res[1], res[2], res[3]};
+            }
+        }
+    }
+}
+
+// Streaming copy of n16 16-byte units (AST output reuse).
+__global__ void __launch_bounds__(256) copy16_kernel(const u32x4* __restrict__ src, u32x4* __restrict__ dst, size_t n16) {
+    const size_t stride = (size_t)gridDim.x * 256 * 4;
+    for (size_t base = (size_t)blockIdx.x * 256 * 4 + threadIdx.x; base < n16; base += stride) {
+        u32x4 v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const size_t i = base + (size_t)u * 256;
+            if (i < n16) v[u] = src[i];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const size_t i = base + (size_t)u * 256;
+            if (i < n16) dst[i] = v[u];
+        }
+    }
+}
+
+template <int D, int MODE>
+hipError_t launch_attn(const AttnLaunch& a, hipStream_t stream) {
+    using G = Geo<D>;
+    Params p{};
+    p.Q = (const uint16_t*)a.Q;
+    p.K = (const uint16_t*)a.K;
+    p.V = (const uint16_t*)a.V;
+    p.Rin = (const float*)a.Rin;
+    p.Rout = (float*)a.Rout;
+    p.ndst = a.ndst;
+    for (int i = 0; i < 4; ++i) p.dst[i] = (uint16_t*)(i < a.ndst ? a.dst[i] : nullptr);
+    p.H = a.H;
+    p.L = a.L;
+    p.w = a.w;
+    p.n_qt = (a.L + BQ - 1) / BQ;
+    const long long nb = (long long)p.n_qt * a.B * a.H;
+    if (nb <= 0 || nb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    p.nblocks = (int)nb;
+    p.c = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
+    const size_t lds = (size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t);
+    if (lds > 65536) {
+        static const hipError_t attr = hipFuncSetAttribute((const void*)attn_kernel<D, MODE>,
+                                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        if (attr != hipSuccess) return attr;
+    }
+    hipLaunchKernelGGL((attn_kernel<D, MODE>), dim3(p.nblocks), dim3(NTHREADS), lds, stream, p);
+    return hipGetLastError();
+}
+
+template <int MODE>
+hipError_t launch_mode(const AttnLaunch& a, hipStream_t stream) {
+    switch (a.d) {
+        case 64: return launch_attn<64, MODE>(a, stream);
+        case 72: return launch_attn<72, MODE>(a, stream);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+bool head_dim_supported(int d) { return d == 64 || d == 72; }
+
+hipError_t launch_full(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_FULL>(a, s); }
+hipError_t launch_refresh(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_REFRESH>(a, s); }
+hipError_t launch_window(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_WINDOW>(a, s); }
+
+hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
+    const size_t n16 = bytes / 16;
+    if (n16 == 0) return hipSuccess;
+    size_t blocks = (n16 + 1023) / 1024;
+    if (blocks > 4096) blocks = 4096;
+    hipLaunchKernelGGL(copy16_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, (const u32x4*)src, (u32x4*)dst, n16);
+    return hipGetLastError();
+}
+
+}  // namespace dfa

@@ -1,0 +1,146 @@
+"""Thin ctypes binding of the C ABI in ``include/dfa.h`` (``libdfa.so``).
+
+Argument marshalling only: each function takes torch tensors, checks that they
+are contiguous [B, H, L, d] tensors on a GPU (bf16, the residual R fp32),
+reads B, H, L, d from the
+shapes, and calls the C function of the same name with the tensors' device
+pointers and the current HIP stream.  All computation happens in the
+library's HIP kernels; there is no fallback of any kind.  A non-OK status
+raises :class:`DfaError` with the library's message.
+
+``lib()`` exposes the raw ctypes handle for callers that marshal pointers
+themselves (the ABI tests do).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from .build import LIB_PATH
+
+DFA_OK, DFA_ERR_INVALID_ARG, DFA_ERR_UNSUPPORTED, DFA_ERR_HIP = 0, 1, 2, 3
+FULL, WARS_REFRESH, WARS_REUSE, AST_REUSE, ASC_REUSE = 0, 1, 2, 3, 4
+CODE_NAMES = {FULL: "FULL", WARS_REFRESH: "WARS_REFRESH", WARS_REUSE: "WARS_REUSE",
+              AST_REUSE: "AST_REUSE", ASC_REUSE: "ASC_REUSE"}
+
+# every symbol include/dfa.h declares
+EXPORTS = ("dfa_attn_full", "dfa_attn_full_and_residual", "dfa_attn_window_plus_residual",
+           "dfa_plan_step", "dfa_plan_make", "dfa_last_error", "dfa_version")
+
+
+class DfaError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"dfa status {status}: {message}")
+        self.status = status
+
+
+_LIB = None
+_vp, _int, _i32p = ctypes.c_void_p, ctypes.c_int, ctypes.POINTER(ctypes.c_int32)
+
+
+def lib() -> ctypes.CDLL:
+    """Load libdfa.so (built in-tree); raises if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it first "
+                               "(python -c 'import __graft_entry__ as g; g.build()')")
+        L = ctypes.CDLL(LIB_PATH)
+        attn = [_vp, _vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _vp]
+        for name in ("dfa_attn_full", "dfa_attn_full_and_residual", "dfa_attn_window_plus_residual"):
+            f = getattr(L, name)
+            f.argtypes = attn
+            f.restype = _int
+        L.dfa_plan_step.argtypes = [_int, _vp, _vp, _vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _vp]
+        L.dfa_plan_step.restype = _int
+        L.dfa_plan_make.argtypes = [ctypes.c_uint64, _int, _int, _int, _int, _i32p, _i32p, _i32p]
+        L.dfa_plan_make.restype = _int
+        L.dfa_last_error.argtypes = []
+        L.dfa_last_error.restype = ctypes.c_char_p
+        L.dfa_version.argtypes = []
+        L.dfa_version.restype = ctypes.c_char_p
+        _LIB = L
+    return _LIB
+
+
+def last_error() -> str:
+    return lib().dfa_last_error().decode()
+
+
+def _check(status: int) -> None:
+    if status != DFA_OK:
+        raise DfaError(status, last_error())
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _shape(*tensors, R=None):
+    import torch
+    ref = tensors[0]
+    for t in (*tensors, R):
+        if t is None:
+            continue
+        want = torch.float32 if t is R else torch.bfloat16
+        if t.dtype != want:
+            raise TypeError(f"expected {want} (R is fp32, the rest bf16), got {t.dtype}")
+        if not t.is_contiguous():
+            raise ValueError("tensors must be contiguous [B, H, L, d]")
+        if t.device.type != "cuda":
+            raise ValueError("tensors must live on a GPU")
+        if t.shape != ref.shape or t.dim() != 4:
+            raise ValueError(f"shape mismatch: {tuple(t.shape)} vs {tuple(ref.shape)}")
+    return tuple(ref.shape)
+
+
+def _stream(stream) -> int:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def dfa_attn_full(Q, K, V, O, w: int = 0, stream=None) -> None:
+    """O = softmax(Q K^T / sqrt(d)) V."""
+    B, H, L, d = _shape(Q, K, V, O)
+    _check(lib().dfa_attn_full(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), None, B, H, L, d, w, _stream(stream)))
+
+
+def dfa_attn_full_and_residual(Q, K, V, O, R, w: int, stream=None) -> None:
+    """O = full attention and R (fp32) = O - window attention (|i-j| <= w)."""
+    B, H, L, d = _shape(Q, K, V, O, R=R)
+    _check(lib().dfa_attn_full_and_residual(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(R), B, H, L, d, w,
+                                            _stream(stream)))
+
+
+def dfa_attn_window_plus_residual(Q, K, V, O, R, w: int, stream=None) -> None:
+    """O = window attention (|i-j| <= w) + R (fp32; None: window attention only)."""
+    B, H, L, d = _shape(Q, K, V, O, R=R)
+    _check(lib().dfa_attn_window_plus_residual(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(R), B, H, L, d, w,
+                                               _stream(stream)))
+
+
+def dfa_plan_step(code: int, Q, K, V, O, R, Ocache, w: int, stream=None) -> None:
+    """One plan entry of one layer (see include/dfa.h for the cache rules)."""
+    B, H, L, d = _shape(O, Q, K, V, Ocache, R=R)
+    _check(lib().dfa_plan_step(int(code), _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(R), _ptr(Ocache),
+                               B, H, L, d, w, _stream(stream)))
+
+
+def dfa_plan_make(seed: int, n_layers: int, n_steps: int, refresh_every: int, B: int):
+    """Seeded plan: int32 arrays (code, r_src, o_src) of shape [n_steps, n_layers]."""
+    shape = (max(n_steps, 0), max(n_layers, 0))
+    code = np.full(shape, -1, dtype=np.int32)
+    r_src = np.full(shape, -1, dtype=np.int32)
+    o_src = np.full(shape, -1, dtype=np.int32)
+    as_p = lambda a: a.ctypes.data_as(_i32p)  # noqa: E731
+    _check(lib().dfa_plan_make(ctypes.c_uint64(seed & (2**64 - 1)), n_layers, n_steps, refresh_every, B,
+                               as_p(code), as_p(r_src), as_p(o_src)))
+    return code, r_src, o_src
+
+
+def version() -> str:
+    return lib().dfa_version().decode()

@@ -1,0 +1,132 @@
+"""The C-ABI library on the host (no GPU): it loads, exports every symbol the
+header declares, rejects bad arguments before touching a device, and its plan
+generator equals the oracle's bit for bit."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import dfa_oracle as orc
+from paper_2406_08552_amd import dfa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dfa.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    return dfa.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dfa_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_binding_exports():
+    assert declared_functions() == sorted(dfa.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+    assert dfa.version().count(".") == 2
+
+
+# Addresses that are never dereferenced: validation fails before any HIP call.
+A, B_, C_, D_, E_ = (0x10000 * (i + 1) for i in range(5))
+
+
+def call_full(L, Q=A, K=B_, V=C_, O=D_, B=2, H=2, L_=64, d=72, w=8):
+    return L.dfa_attn_full(Q, K, V, O, None, B, H, L_, d, w, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(Q=None), dfa.DFA_ERR_INVALID_ARG),
+    (dict(K=None), dfa.DFA_ERR_INVALID_ARG),
+    (dict(O=None), dfa.DFA_ERR_INVALID_ARG),
+    (dict(Q=A + 8), dfa.DFA_ERR_INVALID_ARG),          # misaligned
+    (dict(B=0), dfa.DFA_ERR_INVALID_ARG),
+    (dict(H=-1), dfa.DFA_ERR_INVALID_ARG),
+    (dict(L_=0), dfa.DFA_ERR_INVALID_ARG),
+    (dict(d=0), dfa.DFA_ERR_INVALID_ARG),
+    (dict(w=-1), dfa.DFA_ERR_INVALID_ARG),
+    (dict(d=80), dfa.DFA_ERR_UNSUPPORTED),
+    (dict(d=60), dfa.DFA_ERR_UNSUPPORTED),
+    (dict(O=A), dfa.DFA_ERR_INVALID_ARG),              # O aliases Q
+    (dict(O=B_ + 64), dfa.DFA_ERR_INVALID_ARG),        # O overlaps K
+])
+def test_full_validation(L, kw, status):
+    assert call_full(L, **kw) == status
+    assert dfa.last_error()
+
+
+def test_refresh_validation(L):
+    f = L.dfa_attn_full_and_residual
+    assert f(A, B_, C_, D_, None, 2, 2, 64, 72, 8, None) == dfa.DFA_ERR_INVALID_ARG   # R missing
+    assert f(A, B_, C_, D_, D_, 2, 2, 64, 72, 8, None) == dfa.DFA_ERR_INVALID_ARG     # O == R
+    assert f(A, B_, C_, D_, A, 2, 2, 64, 72, 8, None) == dfa.DFA_ERR_INVALID_ARG      # R aliases Q
+
+
+def test_window_validation(L):
+    f = L.dfa_attn_window_plus_residual
+    assert f(A, B_, C_, D_, D_, 2, 2, 64, 72, 8, None) == dfa.DFA_ERR_INVALID_ARG     # O == R
+    assert f(A, B_, C_, D_, E_ + 4, 2, 2, 64, 72, 8, None) == dfa.DFA_ERR_INVALID_ARG  # misaligned R
+    assert f(A, B_, C_, D_, None, 2, 2, 64, 72, -3, None) == dfa.DFA_ERR_INVALID_ARG
+
+
+def test_plan_step_validation(L):
+    f = L.dfa_plan_step
+    args = (2, 2, 64, 72, 8, None)
+    assert f(7, A, B_, C_, D_, E_, None, *args) == dfa.DFA_ERR_INVALID_ARG            # unknown code
+    assert f(-1, A, B_, C_, D_, E_, None, *args) == dfa.DFA_ERR_INVALID_ARG
+    assert f(dfa.WARS_REFRESH, A, B_, C_, D_, None, None, *args) == dfa.DFA_ERR_INVALID_ARG
+    assert f(dfa.WARS_REUSE, A, B_, C_, D_, None, None, *args) == dfa.DFA_ERR_INVALID_ARG
+    assert f(dfa.AST_REUSE, None, None, None, D_, None, None, *args) == dfa.DFA_ERR_INVALID_ARG
+    assert "Ocache" in dfa.last_error()
+    # AST with the cache equal to O is a no-op: OK without any device work
+    assert f(dfa.AST_REUSE, None, None, None, D_, None, D_, *args) == dfa.DFA_OK
+    assert f(dfa.ASC_REUSE, A, B_, C_, D_, None, None, 3, 2, 64, 72, 8, None) == dfa.DFA_ERR_INVALID_ARG
+    assert "even" in dfa.last_error()
+    assert f(dfa.FULL, A, B_, C_, D_, None, D_ + 32, *args) == dfa.DFA_ERR_INVALID_ARG  # cache overlaps O
+    assert f(dfa.FULL, A, B_, C_, D_, None, A, *args) == dfa.DFA_ERR_INVALID_ARG       # cache aliases Q
+    assert f(dfa.FULL, None, B_, C_, D_, None, None, *args) == dfa.DFA_ERR_INVALID_ARG
+
+
+def test_error_message_is_per_call(L):
+    call_full(L, d=80)
+    assert "d=80" in dfa.last_error()
+    call_full(L, w=-5)
+    assert "w=-5" in dfa.last_error()
+
+
+PLAN_CASES = [(28, 50, 0, 8), (28, 20, 4, 2), (3, 40, 2, 2), (5, 30, 0, 4), (1, 1, 0, 2), (2, 7, 1, 2),
+              (4, 9, 3, 6)]
+
+
+@pytest.mark.parametrize("n_layers,n_steps,every,B", PLAN_CASES)
+def test_plan_bit_equal_to_oracle(n_layers, n_steps, every, B):
+    for seed in list(range(0, 1000, 7)) + [240608552 + 2, 240608552 + 5, 2**64 - 1, 2**63]:
+        ours = dfa.dfa_plan_make(seed, n_layers, n_steps, every, B)
+        ref = orc.plan_make(seed, n_layers, n_steps, every, B)
+        for a, b in zip(ours, ref):
+            assert a.dtype == np.int32 and np.array_equal(a, b), (seed, n_layers, n_steps, every, B)
+
+
+def test_plan_odd_batch_and_bad_dims():
+    with pytest.raises(dfa.DfaError) as e:
+        # 28 x 50 draws contain ASC for this seed
+        dfa.dfa_plan_make(5, 28, 50, 0, 3)
+    assert e.value.status == dfa.DFA_ERR_INVALID_ARG
+    with pytest.raises(ValueError):
+        orc.plan_make(5, 28, 50, 0, 3)
+    for bad in ((0, 5, 0, 2), (5, 0, 0, 2), (5, 5, -1, 2), (5, 5, 0, 0)):
+        with pytest.raises(dfa.DfaError):
+            dfa.dfa_plan_make(1, *bad)
+
+
+def test_plan_null_arrays(L):
+    assert L.dfa_plan_make(ctypes.c_uint64(1), 2, 2, 0, 2, None, None, None) == dfa.DFA_ERR_INVALID_ARG
