@@ -488,6 +488,10 @@ __global__ void __launch_bounds__(NTHREADS) attn_kernel(Params p) {
             float o[4], res[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
+                // R must be the exact difference of the two rounded fp32
+                // results (a band covering every key gives R == 0 exactly):
+                // no fma contraction here.
+#pragma clang fp contract(off)
                 const float win = acc_in.o[qb][mb][i] * inv_in;
                 if constexpr (MODE == MODE_REFRESH) {
                     const float full = (acc_in.o[qb][mb][i] * a_in + acc_out.o[qb][mb][i] * a_out) * inv_full;
