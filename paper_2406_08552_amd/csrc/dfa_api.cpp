@@ -222,7 +222,7 @@ dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, 
             a.dst[a.ndst++] = Ocache;
             a.dst[a.ndst++] = (char*)Ocache + half;
         }
-        return hip_status(dfa::launch_full(a, stream), "ASC launch");
+        return hip_status(dfa::launch_asc(a, stream), "ASC launch");
     }
     if (sep) a.dst[a.ndst++] = Ocache;
     switch (code) {

@@ -23,6 +23,7 @@ struct AttnLaunch {
 
 bool head_dim_supported(int d);
 hipError_t launch_full(const AttnLaunch& a, hipStream_t stream);
+hipError_t launch_asc(const AttnLaunch& a, hipStream_t stream);  // full attention, separate kernel name
 hipError_t launch_refresh(const AttnLaunch& a, hipStream_t stream);
 hipError_t launch_window(const AttnLaunch& a, hipStream_t stream);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);

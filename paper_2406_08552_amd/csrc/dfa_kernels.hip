@@ -10,20 +10,23 @@
 //   A workgroup is 4 wavefronts and owns BQ = 128 consecutive queries of one
 //   (batch, head); each wavefront owns 32 of them (two 16-query MFMA blocks).
 //   The workgroup walks key tiles of BK = 64 keys, staged in LDS with double
-//   buffering (global loads of tile t+1 are in flight while tile t is used).
+//   buffering (global loads of the next tile are in flight while the current
+//   one is used).  Two workgroups share a CU (two wavefronts per SIMD), so the
+//   MFMA work of one overlaps the softmax arithmetic of the other.
 //
 // MFMA mapping (v_mfma_f32_16x16x32_bf16, fp32 accumulation)
 //   Scores are formed transposed, S^T = K Q^T: A = 16 keys x 32 dims from LDS,
 //   B = 32 dims x 16 queries held in registers for the whole kernel.  The
 //   result leaves every lane with a single query (lane % 16) and four keys
 //   per 16-key block, so softmax statistics are per-lane values reduced over
-//   the four lane groups only.  The same registers, rounded to bf16, are
-//   directly the B operand of the second product O^T = V^T P^T, whose A
-//   operand is read from a transposed copy of the V tile in LDS.  The output
-//   accumulator keeps the same one-query-per-lane layout, so the online
-//   softmax rescale needs no data movement.
-//   Head dim 72 = 2 x 32 + 8: the last 8 dims go through one 16x16x16 MFMA
-//   (k padded to 16); PV pads the 72 output dims to 5 blocks of 16.  The
+//   the four 16-lane rows only (two permlane swaps).  The same registers,
+//   rounded to bf16, are directly the B operand of the second product
+//   O^T = V^T P^T, whose A operand is read from a transposed copy of the V
+//   tile in LDS.  The output accumulator keeps the one-query-per-lane
+//   layout, so the online-softmax rescale needs no data movement.
+//   Head dim 72 = 2 x 32 + 8: the last 8 dims go through one more 16x16x32
+//   MFMA with k zero-padded (on gfx950 the k=16 form costs about as much);
+//   PV pads the 72 output dims to 5 blocks of 16.  The
 //   padding row 72 of V^T is set to 1.0, so the PV product also yields the
 //   softmax row sum (the sum of the same bf16 probabilities that weight V).
 //
@@ -33,14 +36,20 @@
 //   exceeds m by more than 8 (so probabilities stay below 2^8 and the
 //   rescale is almost never taken after the first tiles).
 //
-// Band handling
-//   Each wavefront classifies every key tile against its 32 queries: fully
-//   inside the band, fully outside, or straddling it (element mask).  The
-//   window kernel visits only the tiles that intersect the workgroup's band
-//   and skips per wavefront the ones outside it; the refresh kernel sends
-//   inside tiles to the in-band accumulator, outside tiles to the out-of-band
-//   accumulator and splits straddling tiles by element, so every score
-//   feeds exactly one accumulator and K/V are streamed once.
+// Tile walk and band handling
+//   The key tiles a workgroup visits are split into segments so that the hot
+//   loop carries no mask: tiles where every score counts (PLAIN), the ragged
+//   last tile (KEYS: j < L), and the tiles at the band edges, where each
+//   wavefront classifies the tile against its own 32 queries (inside the
+//   band, outside, or straddling it with an element mask).
+//   The window kernel visits only the tiles that intersect the workgroup's
+//   band.  The refresh kernel runs ONE accumulator over two phases: first
+//   the in-band scores of the band tiles (after which the accumulator,
+//   normalised, is the window attention W; it is parked in the R buffer),
+//   then every out-of-band score, which turns the same accumulator into full
+//   attention.  R = O - W is formed in the epilogue.  Every score is used
+//   exactly once, only the few band-edge tiles are visited twice, and no
+//   second accumulator occupies registers.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -50,7 +59,7 @@ namespace dfa {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -64,9 +73,14 @@ constexpr int BQ = NWAVES * QBW * 16;     // queries per workgroup
 constexpr float RESCALE_THRESH = 8.0f;    // lazy rescale margin (log2 units)
 constexpr float NEG_INF = -__builtin_inff();
 
-enum { MODE_FULL = 0, MODE_REFRESH = 1, MODE_WINDOW = 2 };
+enum { MODE_FULL = 0, MODE_REFRESH = 1, MODE_WINDOW = 2, MODE_ASC = 3 };
+// MODE_ASC computes exactly what MODE_FULL computes (on the conditional half of
+// the batch, storing every tile to both halves); it is a separate
+// instantiation only so that profiles report it apart from full attention.
 enum { MASK_NONE = 0, MASK_KEYS = 1, MASK_BAND_IN = 2, MASK_BAND_OUT = 3 };
 enum { TILE_INSIDE = 0, TILE_OUTSIDE = 1, TILE_BOUNDARY = 2 };
+// segment kinds of the tile walk
+enum { SEG_PLAIN = 0, SEG_KEYS = 1, SEG_BAND_IN = 2, SEG_BAND_OUT = 3 };
 
 // Geometry derived from the head dim.
 template <int D>
@@ -75,14 +89,14 @@ struct Geo {
     static_assert(D % 32 == 0 || D % 32 == 8 || D % 32 == 16, "unsupported head dim remainder");
     static constexpr int NC32 = D / 32;              // k=32 chunks of the score product
     static constexpr int D32 = NC32 * 32;
-    static constexpr int TAIL = D - D32;             // dims left for one k=16 chunk (0, 8, 16)
+    static constexpr int TAIL = D - D32;             // dims left for one zero-padded k=32 chunk (0, 8, 16)
     static constexpr int NDB = (D + 15) / 16;        // 16-dim output blocks of PV
     static constexpr int DPV = NDB * 16;             // padded output dims
     static constexpr bool ONES = (D % 16) != 0;      // a padding row of V^T carries ones
     static constexpr int NCH = D / 8;                // 16-byte chunks per row
     // K row pitch in LDS (elements): a 16-byte read by 16 consecutive rows hits
     // 16 distinct 4-bank groups when the pitch in dwords is 4 mod 32.
-    static constexpr int KREAD = (TAIL > 8) ? D32 + 16 : D;
+    static constexpr int KREAD = D;
     static constexpr int KP = ((KREAD / 2 + 27) / 32) * 64 + 8;
     static constexpr int VP = BK + 4;                // V^T row pitch: dwords 2 mod 32
     static constexpr int KS_ELEMS = BK * KP;
@@ -99,7 +113,7 @@ struct Params {
     const uint16_t* K;
     const uint16_t* V;
     const float* Rin;         // MODE_WINDOW: fp32 residual added to the output (or null)
-    float* Rout;              // MODE_REFRESH: fp32 residual output
+    float* Rout;              // MODE_REFRESH: fp32 residual output (also parks W)
     uint16_t* dst[4];         // every destination receives the same output tile
     int ndst;
     int H, L, w;
@@ -109,24 +123,49 @@ struct Params {
 };
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
-__device__ __forceinline__ bf16x4 as_bf16x4(u32x2 v) { return __builtin_bit_cast(bf16x4, v); }
 
-// fp32 -> bf16 with round-to-nearest-even (finite inputs, and +-inf).
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-    return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
+// Two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, bf16x2{(__bf16)lo, (__bf16)hi});
 }
 
-__device__ __forceinline__ float wave_max_groups(float x) {
-    // reduce over the four 16-lane groups that share a query column
-    x = fmaxf(x, __shfl_xor(x, 16));
-    x = fmaxf(x, __shfl_xor(x, 32));
-    return x;
+// s_waitcnt vmcnt(0): every global access of this wavefront has completed.
+// The tile stores sit in branches that whole wavefronts skip; without this
+// the compiler cannot prove at the loop head that the Q fragments have
+// arrived and waits for the just-issued prefetch before the first MFMA.
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Reductions over the four 16-lane rows that hold the same query.
+// v_permlane16_swap exchanges rows 1 and 3 of its first operand with rows 0
+// and 2 of its second; v_permlane32_swap exchanges the upper half of the
+// first with the lower half of the second.  Applied to two copies of x they
+// leave each lane with its own and its partner row's value (rows r^1, then
+// halves r^2).  Issued as inline assembly: the compiler's folding of the
+// builtin's paired result has been seen to drop the second value.  The
+// leading s_nop covers the VALU-write -> permlane-read hazard.
+__device__ __forceinline__ void xchg16(uint32_t& a, uint32_t& b) {
+    asm volatile("s_nop 1\n\tv_permlane16_swap_b32 %0, %1" : "+v"(a), "+v"(b));
+}
+__device__ __forceinline__ void xchg32(uint32_t& a, uint32_t& b) {
+    asm volatile("s_nop 1\n\tv_permlane32_swap_b32 %0, %1" : "+v"(a), "+v"(b));
 }
 
-__device__ __forceinline__ float wave_sum_groups(float x) {
-    x += __shfl_xor(x, 16);
-    x += __shfl_xor(x, 32);
-    return x;
+__device__ __forceinline__ float group_max(float x) {
+    uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+    xchg16(a, b);
+    a = __builtin_bit_cast(uint32_t, fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)));
+    b = a;
+    xchg32(a, b);
+    return fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
+
+__device__ __forceinline__ float group_sum(float x) {
+    uint32_t a = __builtin_bit_cast(uint32_t, x), b = a;
+    xchg16(a, b);
+    a = __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b));
+    b = a;
+    xchg32(a, b);
+    return __builtin_bit_cast(float, a) + __builtin_bit_cast(float, b);
 }
 
 // One score tile, passed by value where a masked private copy is needed.
@@ -151,12 +190,17 @@ struct Acc {
     }
 };
 
+template <int D>
+struct QFrag {
+    bf16x8 a[QBW][Geo<D>::NC32 > 0 ? Geo<D>::NC32 : 1];
+    bf16x8 t[QBW];   // dims D32.. in lane rows g < TAIL/8, zero elsewhere
+};
+
 // Score tile S^T for the wavefront's 32 queries against the 64 keys of one LDS
 // stage: S[qb][kb][i] is the score of query (16*qb + lane%16) and key
 // (16*kb + 4*(lane/16) + i) of the tile.
 template <int D>
-__device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, const bf16x8 (&qa)[QBW][Geo<D>::NC32 > 0 ? Geo<D>::NC32 : 1],
-                                           const bf16x4 (&qt)[QBW], Tile& S, int r, int g) {
+__device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, const QFrag<D>& q, Tile& S, int r, int g) {
     using G = Geo<D>;
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
@@ -164,30 +208,27 @@ __device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, cons
         bf16x8 ka[G::NC32 > 0 ? G::NC32 : 1];
 #pragma unroll
         for (int c = 0; c < G::NC32; ++c) ka[c] = as_bf16x8(*(const u32x4*)(krow + 32 * c + 8 * g));
-        bf16x4 kt = as_bf16x4(u32x2{0u, 0u});
+        u32x4 kt = u32x4{0u, 0u, 0u, 0u};
         if constexpr (G::TAIL > 0) {
-            if (4 * g < G::TAIL) kt = as_bf16x4(*(const u32x2*)(krow + G::D32 + 4 * g));
+            if (8 * g < G::TAIL) kt = *(const u32x4*)(krow + G::D32 + 8 * g);
         }
 #pragma unroll
         for (int qb = 0; qb < QBW; ++qb) {
             f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < G::NC32; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[c], qa[qb][c], s, 0, 0, 0);
-            if constexpr (G::TAIL > 0) s = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(
-                __builtin_bit_cast(__attribute__((ext_vector_type(4))) short, kt),
-                __builtin_bit_cast(__attribute__((ext_vector_type(4))) short, qt[qb]), s, 0, 0, 0);
+            for (int c = 0; c < G::NC32; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[c], q.a[qb][c], s, 0, 0, 0);
+            if constexpr (G::TAIL > 0) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(kt), q.t[qb], s, 0, 0, 0);
             S.s[qb][kb] = s;
         }
     }
 }
 
-// Online-softmax update of one accumulator with one score tile, then PV.
+// Online-softmax update of the accumulator with one score tile, then PV.
 // S is taken by value: the mask is applied to a private copy.
 template <int D, int MASK>
-__device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* __restrict__ Vt,
-                                           int r, int g, int qrow0, int k0, int L, int w, float c) {
+__device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* __restrict__ Vt, int r, int g,
+                                           int qrow0, int k0, int L, int w, float c) {
     using G = Geo<D>;
-    // masking
     if constexpr (MASK != MASK_NONE) {
 #pragma unroll
         for (int qb = 0; qb < QBW; ++qb) {
@@ -207,25 +248,36 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
             }
         }
     }
-    // probabilities, packed to bf16 as the B operand of PV
-    bf16x8 pb[QBW][BK / 32];
+    // tile max per query, and the lazy rescale (one branch for both blocks)
+    float mx[QBW];
+    bool need[QBW];
+    bool need_any = false;
 #pragma unroll
     for (int qb = 0; qb < QBW; ++qb) {
-        float mx = NEG_INF;
+        float v = NEG_INF;
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, S.s[qb][kb][i]);
-        mx = wave_max_groups(mx) * c;
-        const bool need = mx > acc.m[qb] + RESCALE_THRESH;
-        if (__any(need)) {
-            const float mnew = need ? mx : acc.m[qb];
-            const float alpha = need ? __builtin_amdgcn_exp2f(acc.m[qb] - mnew) : 1.0f;
+            for (int i = 0; i < 4; ++i) v = fmaxf(v, S.s[qb][kb][i]);
+        mx[qb] = group_max(v) * c;
+        need[qb] = mx[qb] > acc.m[qb] + RESCALE_THRESH;
+        need_any = need_any || need[qb];
+    }
+    if (__any(need_any)) {
+#pragma unroll
+        for (int qb = 0; qb < QBW; ++qb) {
+            const float mnew = need[qb] ? mx[qb] : acc.m[qb];
+            const float alpha = need[qb] ? __builtin_amdgcn_exp2f(acc.m[qb] - mnew) : 1.0f;
 #pragma unroll
             for (int mb = 0; mb < G::NDB; ++mb) acc.o[qb][mb] *= alpha;
             acc.l[qb] *= alpha;
             acc.m[qb] = mnew;
         }
+    }
+    // probabilities, packed to bf16 as the B operand of PV
+    bf16x8 pb[QBW][BK / 32];
+#pragma unroll
+    for (int qb = 0; qb < QBW; ++qb) {
         const float mbase = acc.m[qb] == NEG_INF ? 0.0f : acc.m[qb];
         float psum = 0.f;
 #pragma unroll
@@ -239,8 +291,8 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
                 const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2], c, -mbase));
                 const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[3], c, -mbase));
                 if constexpr (!G::ONES) psum += (p0 + p1) + (p2 + p3);
-                wds[2 * half + 0] = f32_to_bf16_bits(p0) | (f32_to_bf16_bits(p1) << 16);
-                wds[2 * half + 1] = f32_to_bf16_bits(p2) | (f32_to_bf16_bits(p3) << 16);
+                wds[2 * half + 0] = pack_bf16x2(p0, p1);
+                wds[2 * half + 1] = pack_bf16x2(p2, p3);
             }
             pb[qb][h] = as_bf16x8(u32x4{wds[0], wds[1], wds[2], wds[3]});
         }
@@ -270,7 +322,7 @@ __device__ __forceinline__ float row_sum(const Acc<D>& acc, int qb, int r) {
         constexpr int MB = D / 16, GS = (D % 16) / 4, IS = (D % 16) % 4;
         return __shfl(acc.o[qb][MB][IS], r + 16 * GS);
     } else {
-        return wave_sum_groups(acc.l[qb]);
+        return group_sum(acc.l[qb]);
     }
 }
 
@@ -329,10 +381,76 @@ struct TileLoader {
     }
 };
 
-template <int D, int MODE>
-__global__ void __launch_bounds__(NTHREADS) attn_kernel(Params p) {
+// Per-workgroup state of the tile walk.
+template <int D>
+struct Walk {
     using G = Geo<D>;
-    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+    const uint16_t* Kbh;
+    const uint16_t* Vbh;
+    uint16_t* smem;
+    int tid, r, g, L, w, qw0, qhi_w;
+    bool wave_active;
+    float c;
+    int stage;
+    TileLoader<D> ld;
+
+    // Visit tiles [t0, t1) with one segment kind; `next_after` is the first
+    // tile of the next non-empty segment (-1: none), prefetched while the
+    // last tile of this segment is used.
+    template <int KIND>
+    __device__ __forceinline__ void run(Acc<D>& acc, const QFrag<D>& q, int t0, int t1, int next_after) {
+        for (int t = t0; t < t1; ++t) {
+            const uint16_t* Ks = smem + stage * G::STAGE_ELEMS;
+            const uint16_t* Vt = Ks + G::KS_ELEMS;
+            const int next = (t + 1 < t1) ? t + 1 : next_after;
+            if (next >= 0) ld.load(Kbh, Vbh, next * BK, L, tid);
+            if (wave_active) tile<KIND>(acc, q, Ks, Vt, t * BK);
+            if (next >= 0) {
+                uint16_t* Kn = smem + (stage ^ 1) * G::STAGE_ELEMS;
+                ld.store(Kn, Kn + G::KS_ELEMS, tid);
+            }
+            wait_vm_all();
+            __syncthreads();
+            stage ^= 1;
+        }
+    }
+
+    template <int KIND>
+    __device__ __forceinline__ void tile(Acc<D>& acc, const QFrag<D>& q, const uint16_t* Ks, const uint16_t* Vt,
+                                         int k0) {
+        if constexpr (KIND == SEG_PLAIN) {
+            Tile S;
+            score_tile<D>(Ks, q, S, r, g);
+            accumulate<D, MASK_NONE>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+        } else if constexpr (KIND == SEG_KEYS) {
+            Tile S;
+            score_tile<D>(Ks, q, S, r, g);
+            accumulate<D, MASK_KEYS>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+        } else {
+            // classify the tile against this wavefront's queries
+            const bool ragged = k0 + BK > L;
+            const int khi = min(k0 + BK - 1, L - 1);
+            const int mind = khi < qw0 ? qw0 - khi : (k0 > qhi_w ? k0 - qhi_w : 0);
+            const int maxd = max(qhi_w - k0, khi - qw0);
+            const int cls = maxd <= w ? TILE_INSIDE : (mind > w ? TILE_OUTSIDE : TILE_BOUNDARY);
+            constexpr int SKIP = (KIND == SEG_BAND_IN) ? TILE_OUTSIDE : TILE_INSIDE;
+            if (cls == SKIP) return;
+            Tile S;
+            score_tile<D>(Ks, q, S, r, g);
+            if (cls == TILE_BOUNDARY)
+                accumulate<D, KIND == SEG_BAND_IN ? MASK_BAND_IN : MASK_BAND_OUT>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+            else if (ragged)
+                accumulate<D, MASK_KEYS>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+            else
+                accumulate<D, MASK_NONE>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+        }
+    }
+};
+
+template <int D, int KMODE>
+__device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
+    using G = Geo<D>;
+    constexpr int MODE = KMODE == MODE_ASC ? MODE_FULL : KMODE;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -350,23 +468,11 @@ __global__ void __launch_bounds__(NTHREADS) attn_kernel(Params p) {
     const int L = p.L, w = p.w;
     const size_t head_off = (size_t)bh * L * D;
     const uint16_t* __restrict__ Qbh = p.Q + head_off;
-    const uint16_t* __restrict__ Kbh = p.K + head_off;
-    const uint16_t* __restrict__ Vbh = p.V + head_off;
 
     const int q0 = qt * BQ;                       // workgroup's first query
     const int qw0 = q0 + wave * (QBW * 16);       // wavefront's first query
     const int qhi_wg = min(q0 + BQ - 1, L - 1);
     const int qhi_w = min(qw0 + QBW * 16 - 1, L - 1);
-    const bool wave_active = qw0 < L;
-
-    // key-tile range
-    int t_begin = 0, t_end = (L + BK - 1) / BK;
-    if constexpr (MODE == MODE_WINDOW) {
-        const int klo = max(0, q0 - w);
-        const int khi = (int)min((long long)L - 1, (long long)qhi_wg + w);
-        t_begin = klo / BK;
-        t_end = khi / BK + 1;
-    }
 
     // constant LDS regions of both stages: V^T padding rows (ones row for the
     // row sum, zeros otherwise) and the K pitch padding
@@ -384,8 +490,7 @@ __global__ void __launch_bounds__(NTHREADS) attn_kernel(Params p) {
     }
 
     // Q fragments (B operand of S^T = K Q^T), zero beyond L and beyond d
-    bf16x8 qa[QBW][G::NC32 > 0 ? G::NC32 : 1];
-    bf16x4 qt4[QBW];
+    QFrag<D> q;
 #pragma unroll
     for (int qb = 0; qb < QBW; ++qb) {
         const int qrow = qw0 + 16 * qb + r;
@@ -393,129 +498,151 @@ __global__ void __launch_bounds__(NTHREADS) attn_kernel(Params p) {
         const uint16_t* qp = Qbh + (size_t)(ok ? qrow : 0) * D;
 #pragma unroll
         for (int c = 0; c < G::NC32; ++c)
-            qa[qb][c] = as_bf16x8(ok ? *(const u32x4*)(qp + 32 * c + 8 * g) : u32x4{0u, 0u, 0u, 0u});
-        qt4[qb] = as_bf16x4(u32x2{0u, 0u});
+            q.a[qb][c] = as_bf16x8(ok ? *(const u32x4*)(qp + 32 * c + 8 * g) : u32x4{0u, 0u, 0u, 0u});
+        q.t[qb] = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
         if constexpr (G::TAIL > 0) {
-            if (ok && 4 * g < G::TAIL) qt4[qb] = as_bf16x4(*(const u32x2*)(qp + G::D32 + 4 * g));
+            if (ok && 8 * g < G::TAIL) q.t[qb] = as_bf16x8(*(const u32x4*)(qp + G::D32 + 8 * g));
         }
     }
 
-    Acc<D> acc_in;    // full (MODE_FULL), in-band (REFRESH, WINDOW)
-    Acc<D> acc_out;   // out-of-band (REFRESH only)
-    acc_in.init();
-    if constexpr (MODE == MODE_REFRESH) acc_out.init();
+    Walk<D> wk;
+    wk.Kbh = p.K + head_off;
+    wk.Vbh = p.V + head_off;
+    wk.smem = smem;
+    wk.tid = tid;
+    wk.r = r;
+    wk.g = g;
+    wk.L = L;
+    wk.w = w;
+    wk.qw0 = qw0;
+    wk.qhi_w = qhi_w;
+    wk.wave_active = qw0 < L;
+    wk.c = p.c;
+    wk.stage = 0;
 
-    TileLoader<D> ld;
-    if (t_begin < t_end) {
-        ld.load(Kbh, Vbh, t_begin * BK, L, tid);
-        ld.store(smem, smem + G::KS_ELEMS, tid);
+    // segments of the tile walk
+    const int ntiles = (L + BK - 1) / BK, nfull = L / BK;
+    int tb0 = 0, tb1 = ntiles - 1, m0 = 0, m1 = 0;
+    if constexpr (MODE != MODE_FULL) {
+        const long long klo = max(0LL, (long long)q0 - w);
+        const long long khi = min((long long)L - 1, (long long)qhi_wg + w);
+        tb0 = (int)(klo / BK);
+        tb1 = (int)(khi / BK);
+        // tiles inside the band for every query of the workgroup and not ragged
+        const long long lo_key = (long long)qhi_wg - w;                      // first key every query reaches
+        const long long hi_key = min((long long)q0 + w, (long long)L - 1);  // last key every query reaches
+        const long long ai0 = lo_key <= 0 ? 0 : (lo_key + BK - 1) / BK;
+        const long long ai1 = hi_key - (BK - 1) < 0 ? -1 : (hi_key - (BK - 1)) / BK;
+        m0 = (int)min(max(ai0, (long long)tb0), (long long)tb1 + 1);
+        m1 = (int)min(max(ai1 + 1, (long long)m0), (long long)tb1 + 1);
     }
+    constexpr int NSEG = MODE == MODE_FULL ? 2 : (MODE == MODE_WINDOW ? 3 : 8);
+    int s0[NSEG], s1[NSEG];
+    if constexpr (MODE == MODE_FULL) {
+        s0[0] = 0; s1[0] = nfull;              // PLAIN
+        s0[1] = nfull; s1[1] = ntiles;         // KEYS
+    } else {
+        s0[0] = tb0; s1[0] = m0;               // BAND_IN
+        s0[1] = m0; s1[1] = m1;                // PLAIN
+        s0[2] = m1; s1[2] = tb1 + 1;           // BAND_IN
+        if constexpr (MODE == MODE_REFRESH) {
+            const int after = max(tb1 + 1, nfull);
+            s0[3] = 0; s1[3] = tb0;            // PLAIN (left of the band)
+            s0[4] = tb0; s1[4] = m0;           // BAND_OUT
+            s0[5] = m1; s1[5] = tb1 + 1;       // BAND_OUT
+            s0[6] = tb1 + 1; s1[6] = after;    // PLAIN (right of the band)
+            s0[7] = after; s1[7] = ntiles;     // KEYS (ragged tile right of the band)
+        }
+    }
+    // first tile of the first non-empty segment at or after each position
+    int nxt[NSEG + 1];
+    nxt[NSEG] = -1;
+#pragma unroll
+    for (int i = NSEG - 1; i >= 0; --i) nxt[i] = s0[i] < s1[i] ? s0[i] : nxt[i + 1];
+
+    Acc<D> acc;
+    acc.init();
+
+    // every workgroup has at least one key tile: the window of any query
+    // contains the query itself
+    wk.ld.load(wk.Kbh, wk.Vbh, nxt[0] * BK, L, tid);
+    wk.ld.store(smem, smem + G::KS_ELEMS, tid);
+    wait_vm_all();
     __syncthreads();
 
-    for (int t = t_begin; t < t_end; ++t) {
-        const int stage = (t - t_begin) & 1;
-        const uint16_t* Ks = smem + stage * G::STAGE_ELEMS;
-        const uint16_t* Vt = Ks + G::KS_ELEMS;
-        const bool has_next = t + 1 < t_end;
-        if (has_next) ld.load(Kbh, Vbh, (t + 1) * BK, L, tid);
+    if constexpr (MODE == MODE_FULL) {
+        wk.template run<SEG_PLAIN>(acc, q, s0[0], s1[0], nxt[1]);
+        wk.template run<SEG_KEYS>(acc, q, s0[1], s1[1], nxt[2]);
+    } else {
+        wk.template run<SEG_BAND_IN>(acc, q, s0[0], s1[0], nxt[1]);
+        wk.template run<SEG_PLAIN>(acc, q, s0[1], s1[1], nxt[2]);
+        wk.template run<SEG_BAND_IN>(acc, q, s0[2], s1[2], nxt[3]);
+    }
 
-        const int k0 = t * BK;
-        if (wave_active) {
-            const int khi = min(k0 + BK - 1, L - 1);
-            const bool ragged = k0 + BK > L;
-            int cls = TILE_INSIDE;
-            if constexpr (MODE != MODE_FULL) {
-                const int mind = khi < qw0 ? qw0 - khi : (k0 > qhi_w ? k0 - qhi_w : 0);
-                const int maxd = max(qhi_w - k0, khi - qw0);
-                cls = maxd <= w ? TILE_INSIDE : (mind > w ? TILE_OUTSIDE : TILE_BOUNDARY);
-            }
-            if (MODE != MODE_WINDOW || cls != TILE_OUTSIDE) {
-                Tile S;
-                score_tile<D>(Ks, qa, qt4, S, r, g);
-                if constexpr (MODE == MODE_FULL) {
-                    if (ragged) accumulate<D, MASK_KEYS>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
-                    else accumulate<D, MASK_NONE>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
-                } else if constexpr (MODE == MODE_WINDOW) {
-                    if (cls == TILE_BOUNDARY) accumulate<D, MASK_BAND_IN>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
-                    else if (ragged) accumulate<D, MASK_KEYS>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
-                    else accumulate<D, MASK_NONE>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
-                } else {
-                    if (cls == TILE_BOUNDARY) {
-                        accumulate<D, MASK_BAND_IN>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
-                        accumulate<D, MASK_BAND_OUT>(acc_out, S, Vt, r, g, qw0, k0, L, w, p.c);
-                    } else if (cls == TILE_INSIDE) {
-                        if (ragged) accumulate<D, MASK_KEYS>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
-                        else accumulate<D, MASK_NONE>(acc_in, S, Vt, r, g, qw0, k0, L, w, p.c);
-                    } else {
-                        if (ragged) accumulate<D, MASK_KEYS>(acc_out, S, Vt, r, g, qw0, k0, L, w, p.c);
-                        else accumulate<D, MASK_NONE>(acc_out, S, Vt, r, g, qw0, k0, L, w, p.c);
+    if constexpr (MODE == MODE_REFRESH) {
+        // the accumulator now holds the window attention of the wavefront's
+        // queries: park W (fp32) in the R buffer
+        if (wk.wave_active) {
+#pragma unroll
+            for (int qb = 0; qb < QBW; ++qb) {
+                const int qrow = qw0 + 16 * qb + r;
+                const float inv = 1.f / row_sum<D>(acc, qb, r);
+                if (qrow < L) {
+#pragma unroll
+                    for (int mb = 0; mb < G::NDB; ++mb) {
+                        const int col = 16 * mb + 4 * g;
+                        if (col < D) *(f32x4*)(p.Rout + head_off + (size_t)qrow * D + col) = acc.o[qb][mb] * inv;
                     }
                 }
             }
         }
-
-        if (has_next) {
-            uint16_t* Kn = smem + (stage ^ 1) * G::STAGE_ELEMS;
-            ld.store(Kn, Kn + G::KS_ELEMS, tid);
-        }
-        __syncthreads();
+        wk.template run<SEG_PLAIN>(acc, q, s0[3], s1[3], nxt[4]);
+        wk.template run<SEG_BAND_OUT>(acc, q, s0[4], s1[4], nxt[5]);
+        wk.template run<SEG_BAND_OUT>(acc, q, s0[5], s1[5], nxt[6]);
+        wk.template run<SEG_PLAIN>(acc, q, s0[6], s1[6], nxt[7]);
+        wk.template run<SEG_KEYS>(acc, q, s0[7], s1[7], nxt[8]);
     }
 
-    if (!wave_active) return;
+    if (!wk.wave_active) return;
 
-    // epilogue: normalise, combine, store bf16 to every destination
+    // epilogue: normalise, form R, store bf16 to every destination
 #pragma unroll
     for (int qb = 0; qb < QBW; ++qb) {
         const int qrow = qw0 + 16 * qb + r;
-        const float l_in = row_sum<D>(acc_in, qb, r);
-        float a_in = 1.f, a_out = 0.f, inv_full = 0.f;
-        if constexpr (MODE == MODE_REFRESH) {
-            const float l_out = row_sum<D>(acc_out, qb, r);
-            const float m_in = acc_in.m[qb], m_out = acc_out.m[qb];
-            const float M = fmaxf(m_in, m_out);
-            a_in = (m_in == M) ? 1.f : __builtin_amdgcn_exp2f(m_in - M);
-            a_out = (m_out == NEG_INF) ? 0.f : ((m_out == M) ? 1.f : __builtin_amdgcn_exp2f(m_out - M));
-            inv_full = 1.f / (l_in * a_in + l_out * a_out);
-        }
-        const float inv_in = 1.f / l_in;
+        const float inv = 1.f / row_sum<D>(acc, qb, r);
         if (qrow >= L) continue;
         const size_t row_off = head_off + (size_t)qrow * D;
 #pragma unroll
         for (int mb = 0; mb < G::NDB; ++mb) {
+            // no fma contraction: o must be rounded exactly as the parked W was
+#pragma clang fp contract(off)
             const int col = 16 * mb + 4 * g;
             if (col >= D) continue;
             const size_t off = row_off + col;
-            float o[4], res[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                // R must be the exact difference of the two rounded fp32
-                // results (a band covering every key gives R == 0 exactly):
-                // no fma contraction here.
-#pragma clang fp contract(off)
-                const float win = acc_in.o[qb][mb][i] * inv_in;
-                if constexpr (MODE == MODE_REFRESH) {
-                    const float full = (acc_in.o[qb][mb][i] * a_in + acc_out.o[qb][mb][i] * a_out) * inv_full;
-                    o[i] = full;
-                    res[i] = full - win;
-                } else {
-                    o[i] = win;
-                }
+            const f32x4 o = acc.o[qb][mb] * inv;
+            f32x4 out = o;
+            if constexpr (MODE == MODE_REFRESH) {
+                // R is the exact difference of the two rounded fp32 results (a
+                // band covering every key gives R == 0 exactly); the window
+                // result parked above is read back by the lane that wrote it.
+                const f32x4 win = *(const f32x4*)(p.Rout + off);
+                *(f32x4*)(p.Rout + off) = o - win;
             }
             if constexpr (MODE == MODE_WINDOW) {
-                if (p.Rin) {
-                    const f32x4 rv = *(const f32x4*)(p.Rin + off);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) o[i] += rv[i];
-                }
+                if (p.Rin) out = o + *(const f32x4*)(p.Rin + off);
             }
-            const u32x2 ov = u32x2{f32_to_bf16_bits(o[0]) | (f32_to_bf16_bits(o[1]) << 16),
-                                   f32_to_bf16_bits(o[2]) | (f32_to_bf16_bits(o[3]) << 16)};
+            const u32x2 ov = u32x2{pack_bf16x2(out[0], out[1]), pack_bf16x2(out[2], out[3])};
             for (int di = 0; di < p.ndst; ++di) *(u32x2*)(p.dst[di] + off) = ov;
-            if constexpr (MODE == MODE_REFRESH) {
-                *(f32x4*)(p.Rout + off) = f32x4{res[0], res[1], res[2], res[3]};
-            }
         }
     }
+}
+
+// Two waves per SIMD (register budget 256): the MFMA work of one wavefront
+// overlaps the softmax arithmetic of the other.
+template <int D, int MODE>
+__global__ void __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) attn_kernel(Params p) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+    attn_body<D, MODE>(p, smem);
 }
 
 // Streaming copy of n16 16-byte units (AST output reuse).
@@ -555,12 +682,8 @@ hipError_t launch_attn(const AttnLaunch& a, hipStream_t stream) {
     if (nb <= 0 || nb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
     p.nblocks = (int)nb;
     p.c = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-    const size_t lds = (size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t);
-    if (lds > 65536) {
-        static const hipError_t attr = hipFuncSetAttribute((const void*)attn_kernel<D, MODE>,
-                                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-        if (attr != hipSuccess) return attr;
-    }
+    constexpr size_t lds = (size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t);
+    static_assert(lds <= 65536, "LDS above the default dynamic limit");
     hipLaunchKernelGGL((attn_kernel<D, MODE>), dim3(p.nblocks), dim3(NTHREADS), lds, stream, p);
     return hipGetLastError();
 }
@@ -579,6 +702,7 @@ hipError_t launch_mode(const AttnLaunch& a, hipStream_t stream) {
 bool head_dim_supported(int d) { return d == 64 || d == 72; }
 
 hipError_t launch_full(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_FULL>(a, s); }
+hipError_t launch_asc(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_ASC>(a, s); }
 hipError_t launch_refresh(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_REFRESH>(a, s); }
 hipError_t launch_window(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_WINDOW>(a, s); }
 
