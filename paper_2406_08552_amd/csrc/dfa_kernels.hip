@@ -60,6 +60,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -83,29 +85,34 @@ enum { TILE_INSIDE = 0, TILE_OUTSIDE = 1, TILE_BOUNDARY = 2 };
 enum { SEG_PLAIN = 0, SEG_KEYS = 1, SEG_BAND_IN = 2, SEG_BAND_OUT = 3 };
 
 // Geometry derived from the head dim.
+//   LDS tiles are row-major, one key per row, filled by 16-byte direct
+//   global->LDS copies (lane l of a copy lands at base + 16 l, so chunk c of a
+//   tile sits at 16 c bytes).  K rows take KPC chunks (pitch 144 B for d = 64
+//   and 72: 16-byte reads by 16 consecutive rows hit distinct 4-bank groups).
+//   V rows take VPC chunks; for d = 72 the tenth chunk holds (1, 0, ..., 0),
+//   a constant "dim 72 = 1" column that makes the PV product emit the row
+//   sum.  Chunks at or beyond NCH are never copied into.
 template <int D>
 struct Geo {
-    static_assert(D % 8 == 0 && D <= 128, "head dim must be a multiple of 8, at most 128");
+    static_assert(D % 8 == 0 && D <= 72, "head dim must be a multiple of 8, at most 72");
     static_assert(D % 32 == 0 || D % 32 == 8 || D % 32 == 16, "unsupported head dim remainder");
     static constexpr int NC32 = D / 32;              // k=32 chunks of the score product
     static constexpr int D32 = NC32 * 32;
     static constexpr int TAIL = D - D32;             // dims left for one zero-padded k=32 chunk (0, 8, 16)
     static constexpr int NDB = (D + 15) / 16;        // 16-dim output blocks of PV
-    static constexpr int DPV = NDB * 16;             // padded output dims
-    static constexpr bool ONES = (D % 16) != 0;      // a padding row of V^T carries ones
-    static constexpr int NCH = D / 8;                // 16-byte chunks per row
-    // K row pitch in LDS (elements): a 16-byte read by 16 consecutive rows hits
-    // 16 distinct 4-bank groups when the pitch in dwords is 4 mod 32.
-    static constexpr int KREAD = D;
-    static constexpr int KP = ((KREAD / 2 + 27) / 32) * 64 + 8;
-    static constexpr int VP = BK + 4;                // V^T row pitch: dwords 2 mod 32
+    static constexpr bool ONES = (D % 16) != 0;      // the padding column D of V carries ones
+    static constexpr int NCH = D / 8;                // 16-byte chunks of data per row
+    static constexpr int KPC = 9;                    // K row pitch in chunks (144 B)
+    static constexpr int VPC = ONES ? NCH + 1 : 9;   // V row pitch in chunks (160 B for d = 72)
+    static constexpr int KP = KPC * 8;               // pitches in elements
+    static constexpr int VP = VPC * 8;
     static constexpr int KS_ELEMS = BK * KP;
-    static constexpr int VS_ELEMS = DPV * VP;
+    static constexpr int VS_ELEMS = BK * VP;
     static constexpr int STAGE_ELEMS = KS_ELEMS + VS_ELEMS;
-    static constexpr int KLOADS = (BK * NCH + NTHREADS - 1) / NTHREADS;
-    static constexpr int VITEMS = (BK / 4) * NCH;    // (4-key group, chunk) work items
-    static_assert(VITEMS <= NTHREADS, "V tile needs more than one item per thread");
-    static_assert((KP / 2) % 32 == 4 && KP >= KREAD, "K pitch");
+    static constexpr int KROUNDS = (BK * KPC + NTHREADS - 1) / NTHREADS;
+    static constexpr int VROUNDS = (BK * VPC + NTHREADS - 1) / NTHREADS;
+    static_assert(NDB * 16 <= VP, "PV reads the padded dims of each V row");
+    static_assert((KP / 2) % 32 == 4, "K pitch");
 };
 
 struct Params {
@@ -226,7 +233,7 @@ __device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, cons
 // Online-softmax update of the accumulator with one score tile, then PV.
 // S is taken by value: the mask is applied to a private copy.
 template <int D, int MASK>
-__device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* __restrict__ Vt, int r, int g,
+__device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* Vs, int r, int g,
                                            int qrow0, int k0, int L, int w, float c) {
     using G = Geo<D>;
     if constexpr (MASK != MASK_NONE) {
@@ -298,15 +305,20 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
         }
         if constexpr (!G::ONES) acc.l[qb] += psum;
     }
-    // O^T += V^T P^T
+    // O^T += V^T P^T.  The A operand (16 dims x 32 keys) comes from the
+    // row-major V tile through transposing reads: within each 16-lane row,
+    // lane 4m+q addresses dims 16mb+4q..+3 of key k+m, and every lane receives
+    // its own dim of keys k..k+3.
+    const int tm = r >> 2, tq = r & 3;
 #pragma unroll
     for (int h = 0; h < BK / 32; ++h) {
 #pragma unroll
         for (int mb = 0; mb < G::NDB; ++mb) {
-            const uint16_t* vrow = Vt + (16 * mb + r) * G::VP + 32 * h + 4 * g;
-            const u32x2 v0 = *(const u32x2*)(vrow);
-            const u32x2 v1 = *(const u32x2*)(vrow + 16);
-            const bf16x8 va = as_bf16x8(u32x4{v0[0], v0[1], v1[0], v1[1]});
+            const uint16_t* src = Vs + (32 * h + 4 * g + tm) * G::VP + 16 * mb + 4 * tq;
+            const s16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(src));
+            const s16x4 v1 =
+                __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(src + 16 * G::VP));
+            const bf16x8 va = __builtin_bit_cast(bf16x8, s16x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
 #pragma unroll
             for (int qb = 0; qb < QBW; ++qb)
                 acc.o[qb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[qb][h], acc.o[qb][mb], 0, 0, 0);
@@ -326,60 +338,37 @@ __device__ __forceinline__ float row_sum(const Acc<D>& acc, int qb, int r) {
     }
 }
 
-// Global -> register prefetch of one K/V tile, and register -> LDS store.
+// Direct global -> LDS copy of one K/V tile (no staging registers).  Rows
+// beyond L copy row L-1 instead: their scores are masked and their
+// probabilities are zero, so any finite value will do.
 template <int D>
-struct TileLoader {
+__device__ __forceinline__ void issue_tile(const uint16_t* __restrict__ Kbh, const uint16_t* __restrict__ Vbh, int k0,
+                                           int L, int tid, uint16_t* Ks, uint16_t* Vs) {
     using G = Geo<D>;
-    u32x4 kreg[G::KLOADS];
-    u32x4 vreg[4];
-
-    __device__ __forceinline__ void load(const uint16_t* __restrict__ Kbh, const uint16_t* __restrict__ Vbh, int k0, int L,
-                                         int tid) {
+    const int wave_chunk0 = tid & ~63;   // first chunk of this wavefront in a round
 #pragma unroll
-        for (int it = 0; it < G::KLOADS; ++it) {
-            const int cidx = tid + it * NTHREADS;
-            const int row = cidx / G::NCH, ch = cidx % G::NCH;
-            kreg[it] = u32x4{0u, 0u, 0u, 0u};
-            if (cidx < BK * G::NCH && k0 + row < L)
-                kreg[it] = *(const u32x4*)(Kbh + (size_t)(k0 + row) * D + ch * 8);
-        }
-        if (tid < G::VITEMS) {
-            const int kg = tid / G::NCH, ch = tid % G::NCH;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int row = 4 * kg + e;
-                vreg[e] = u32x4{0u, 0u, 0u, 0u};
-                if (k0 + row < L) vreg[e] = *(const u32x4*)(Vbh + (size_t)(k0 + row) * D + ch * 8);
-            }
+    for (int it = 0; it < G::KROUNDS; ++it) {
+        const int c = it * NTHREADS + tid;
+        const int row = c / G::KPC, ch = c % G::KPC;
+        if (row < BK && ch < G::NCH) {
+            const int krow = min(k0 + row, L - 1);
+            __builtin_amdgcn_global_load_lds((const void*)(Kbh + (size_t)krow * D + ch * 8),
+                                             (__attribute__((address_space(3))) void*)(Ks + (it * NTHREADS + wave_chunk0) * 8),
+                                             16, 0, 0);
         }
     }
-
-    __device__ __forceinline__ void store(uint16_t* __restrict__ Ks, uint16_t* __restrict__ Vt, int tid) const {
 #pragma unroll
-        for (int it = 0; it < G::KLOADS; ++it) {
-            const int cidx = tid + it * NTHREADS;
-            const int row = cidx / G::NCH, ch = cidx % G::NCH;
-            if (cidx < BK * G::NCH) *(u32x4*)(Ks + row * G::KP + ch * 8) = kreg[it];
-        }
-        if (tid < G::VITEMS) {
-            const int kg = tid / G::NCH, ch = tid % G::NCH;
-            // transpose 4 keys x 8 dims into 8 rows (dims) x 4 keys
-#pragma unroll
-            for (int cc = 0; cc < 8; ++cc) {
-                const int wi = cc >> 1;
-                uint32_t lo, hi;
-                if (cc & 1) {
-                    lo = (vreg[0][wi] >> 16) | (vreg[1][wi] & 0xFFFF0000u);
-                    hi = (vreg[2][wi] >> 16) | (vreg[3][wi] & 0xFFFF0000u);
-                } else {
-                    lo = (vreg[0][wi] & 0xFFFFu) | (vreg[1][wi] << 16);
-                    hi = (vreg[2][wi] & 0xFFFFu) | (vreg[3][wi] << 16);
-                }
-                *(u32x2*)(Vt + (8 * ch + cc) * G::VP + 4 * kg) = u32x2{lo, hi};
-            }
+    for (int it = 0; it < G::VROUNDS; ++it) {
+        const int c = it * NTHREADS + tid;
+        const int row = c / G::VPC, ch = c % G::VPC;
+        if (row < BK && ch < G::NCH) {
+            const int vrow = min(k0 + row, L - 1);
+            __builtin_amdgcn_global_load_lds((const void*)(Vbh + (size_t)vrow * D + ch * 8),
+                                             (__attribute__((address_space(3))) void*)(Vs + (it * NTHREADS + wave_chunk0) * 8),
+                                             16, 0, 0);
         }
     }
-};
+}
 
 // Per-workgroup state of the tile walk.
 template <int D>
@@ -392,7 +381,6 @@ struct Walk {
     bool wave_active;
     float c;
     int stage;
-    TileLoader<D> ld;
 
     // Visit tiles [t0, t1) with one segment kind; `next_after` is the first
     // tile of the next non-empty segment (-1: none), prefetched while the
@@ -401,14 +389,13 @@ struct Walk {
     __device__ __forceinline__ void run(Acc<D>& acc, const QFrag<D>& q, int t0, int t1, int next_after) {
         for (int t = t0; t < t1; ++t) {
             const uint16_t* Ks = smem + stage * G::STAGE_ELEMS;
-            const uint16_t* Vt = Ks + G::KS_ELEMS;
+            const uint16_t* Vs = Ks + G::KS_ELEMS;
             const int next = (t + 1 < t1) ? t + 1 : next_after;
-            if (next >= 0) ld.load(Kbh, Vbh, next * BK, L, tid);
-            if (wave_active) tile<KIND>(acc, q, Ks, Vt, t * BK);
             if (next >= 0) {
                 uint16_t* Kn = smem + (stage ^ 1) * G::STAGE_ELEMS;
-                ld.store(Kn, Kn + G::KS_ELEMS, tid);
+                issue_tile<D>(Kbh, Vbh, next * BK, L, tid, Kn, Kn + G::KS_ELEMS);
             }
+            if (wave_active) tile<KIND>(acc, q, Ks, Vs, t * BK);
             wait_vm_all();
             __syncthreads();
             stage ^= 1;
@@ -416,16 +403,16 @@ struct Walk {
     }
 
     template <int KIND>
-    __device__ __forceinline__ void tile(Acc<D>& acc, const QFrag<D>& q, const uint16_t* Ks, const uint16_t* Vt,
+    __device__ __forceinline__ void tile(Acc<D>& acc, const QFrag<D>& q, const uint16_t* Ks, const uint16_t* Vs,
                                          int k0) {
         if constexpr (KIND == SEG_PLAIN) {
             Tile S;
             score_tile<D>(Ks, q, S, r, g);
-            accumulate<D, MASK_NONE>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+            accumulate<D, MASK_NONE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
         } else if constexpr (KIND == SEG_KEYS) {
             Tile S;
             score_tile<D>(Ks, q, S, r, g);
-            accumulate<D, MASK_KEYS>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+            accumulate<D, MASK_KEYS>(acc, S, Vs, r, g, qw0, k0, L, w, c);
         } else {
             // classify the tile against this wavefront's queries
             const bool ragged = k0 + BK > L;
@@ -438,11 +425,11 @@ struct Walk {
             Tile S;
             score_tile<D>(Ks, q, S, r, g);
             if (cls == TILE_BOUNDARY)
-                accumulate<D, KIND == SEG_BAND_IN ? MASK_BAND_IN : MASK_BAND_OUT>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+                accumulate<D, KIND == SEG_BAND_IN ? MASK_BAND_IN : MASK_BAND_OUT>(acc, S, Vs, r, g, qw0, k0, L, w, c);
             else if (ragged)
-                accumulate<D, MASK_KEYS>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+                accumulate<D, MASK_KEYS>(acc, S, Vs, r, g, qw0, k0, L, w, c);
             else
-                accumulate<D, MASK_NONE>(acc, S, Vt, r, g, qw0, k0, L, w, c);
+                accumulate<D, MASK_NONE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
         }
     }
 };
@@ -474,18 +461,12 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     const int qhi_wg = min(q0 + BQ - 1, L - 1);
     const int qhi_w = min(qw0 + QBW * 16 - 1, L - 1);
 
-    // constant LDS regions of both stages: V^T padding rows (ones row for the
-    // row sum, zeros otherwise) and the K pitch padding
-    for (int st = 0; st < 2; ++st) {
-        uint16_t* Ks = smem + st * G::STAGE_ELEMS;
-        uint16_t* Vt = Ks + G::KS_ELEMS;
-        for (int idx = tid; idx < (G::DPV - D) * G::VP; idx += NTHREADS) {
-            const int row = D + idx / G::VP;
-            Vt[row * G::VP + idx % G::VP] = (G::ONES && row == D) ? (uint16_t)0x3F80u : (uint16_t)0u;
-        }
-        if constexpr (G::KP > D) {
-            for (int idx = tid; idx < BK * (G::KP - D); idx += NTHREADS)
-                Ks[(idx / (G::KP - D)) * G::KP + D + idx % (G::KP - D)] = 0;
+    // constant V padding chunk of every row in both stages: (1, 0, ..., 0) for
+    // the row-sum column, never overwritten by the tile copies
+    if constexpr (G::ONES) {
+        for (int idx = tid; idx < 2 * BK * 8; idx += NTHREADS) {
+            const int st = idx / (BK * 8), row = (idx / 8) % BK, e = idx % 8;
+            smem[st * G::STAGE_ELEMS + G::KS_ELEMS + row * G::VP + D + e] = (e == 0) ? (uint16_t)0x3F80u : (uint16_t)0u;
         }
     }
 
@@ -565,8 +546,7 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
 
     // every workgroup has at least one key tile: the window of any query
     // contains the query itself
-    wk.ld.load(wk.Kbh, wk.Vbh, nxt[0] * BK, L, tid);
-    wk.ld.store(smem, smem + G::KS_ELEMS, tid);
+    issue_tile<D>(wk.Kbh, wk.Vbh, nxt[0] * BK, L, tid, smem, smem + G::KS_ELEMS);
     wait_vm_all();
     __syncthreads();
 
@@ -641,7 +621,7 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
 // overlaps the softmax arithmetic of the other.
 template <int D, int MODE>
 __global__ void __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) attn_kernel(Params p) {
-    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * Geo<D>::STAGE_ELEMS];
     attn_body<D, MODE>(p, smem);
 }
 
@@ -682,9 +662,8 @@ hipError_t launch_attn(const AttnLaunch& a, hipStream_t stream) {
     if (nb <= 0 || nb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
     p.nblocks = (int)nb;
     p.c = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-    constexpr size_t lds = (size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t);
-    static_assert(lds <= 65536, "LDS above the default dynamic limit");
-    hipLaunchKernelGGL((attn_kernel<D, MODE>), dim3(p.nblocks), dim3(NTHREADS), lds, stream, p);
+    static_assert((size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t) <= 80 * 1024, "two workgroups per CU must fit in LDS");
+    hipLaunchKernelGGL((attn_kernel<D, MODE>), dim3(p.nblocks), dim3(NTHREADS), 0, stream, p);
     return hipGetLastError();
 }
 
