@@ -620,7 +620,7 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
 // Two waves per SIMD (register budget 256): the MFMA work of one wavefront
 // overlaps the softmax arithmetic of the other.
 template <int D, int MODE>
-__global__ void __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(2, 2))) attn_kernel(Params p) {
+__global__ void __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(3, 3))) attn_kernel(Params p) {
     __shared__ __attribute__((aligned(16))) uint16_t smem[2 * Geo<D>::STAGE_ELEMS];
     attn_body<D, MODE>(p, smem);
 }
