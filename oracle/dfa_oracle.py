@@ -39,10 +39,13 @@ from __future__ import annotations
 
 import numpy as np
 
-# Plan codes (one per strategy a layer may run at a step).
+# Plan codes (one per strategy a layer may run at a step).  Codes 5 and 6 are
+# the combined WA-RS + ASC strategy of the strategy list in Sec. 3.5.
 FULL, WARS_REFRESH, WARS_REUSE, AST_REUSE, ASC_REUSE = 0, 1, 2, 3, 4
+WARS_ASC_REFRESH, WARS_ASC_REUSE = 5, 6
 CODE_NAMES = {FULL: "FULL", WARS_REFRESH: "WARS_REFRESH", WARS_REUSE: "WARS_REUSE",
-              AST_REUSE: "AST_REUSE", ASC_REUSE: "ASC_REUSE"}
+              AST_REUSE: "AST_REUSE", ASC_REUSE: "ASC_REUSE",
+              WARS_ASC_REFRESH: "WARS_ASC_REFRESH", WARS_ASC_REUSE: "WARS_ASC_REUSE"}
 
 _ROW_BLOCK = 1024  # query rows per block: bounds the fp64 score block at 1024 x L
 
@@ -169,6 +172,32 @@ def asc_reuse(Q, K, V) -> np.ndarray:
     return np.concatenate([O_cond, O_cond], axis=0)
 
 
+def _cond_half(B: int) -> int:
+    if B % 2:
+        raise ValueError("WA-RS + ASC needs an even batch (conditional/unconditional pairs)")
+    return B // 2
+
+
+def wars_asc_refresh(Q, K, V, w: int):
+    """WA-RS and ASC at once (strategy list of Sec. 3.5; Table 2's WA-RS+ASC
+    row), first step of a residual-sharing set: Eq. (1) is evaluated on the
+    conditional half only and its output is reused for the unconditional
+    half (Sec. 3.4).  Returns (O, R_cond) where O is the whole batch and
+    R_cond = O_r - W_r holds the conditional entries 0..B/2-1 only."""
+    half = _cond_half(np.shape(Q)[0])
+    Oc, Rc = wars_refresh(np.asarray(Q)[:half], np.asarray(K)[:half], np.asarray(V)[:half], w)
+    return np.concatenate([Oc, Oc], axis=0), Rc
+
+
+def wars_asc_reuse(Q, K, V, R_cond, w: int) -> np.ndarray:
+    """WA-RS and ASC at once, later step of the set: Eq. (2) on the conditional
+    half with the conditional residual R_cond ([B/2, H, L, d]), and the
+    result reused for the unconditional half."""
+    half = _cond_half(np.shape(Q)[0])
+    Oc = wars_reuse(np.asarray(Q)[:half], np.asarray(K)[:half], np.asarray(V)[:half], R_cond, w)
+    return np.concatenate([Oc, Oc], axis=0)
+
+
 # ---------------------------------------------------------------------------
 # Brute force (explicit loops) -- used only on tiny inputs, as an independent pin
 # ---------------------------------------------------------------------------
@@ -279,12 +308,16 @@ def fixed_plan(codes, n_layers: int = 1):
     r_src = np.full_like(code, -1)
     o_src = np.full_like(code, -1)
     for layer in range(n_layers):
-        last_refresh, cache_step = -1, -1
+        last_refresh, cache_step, half_r = -1, -1, False
         for t in range(n_steps):
             c = int(code[t, layer])
-            if c == WARS_REUSE:
+            if c not in CODE_NAMES:
+                raise ValueError(f"unknown plan code {c}")
+            if c in (WARS_REUSE, WARS_ASC_REUSE):
                 if last_refresh < 0:
                     raise ValueError("reuse before any refresh")
+                if c == WARS_REUSE and half_r:
+                    raise ValueError("whole-batch reuse after a conditional-half refresh")
                 r_src[t, layer] = last_refresh
             if c == AST_REUSE:
                 if cache_step < 0:
@@ -293,44 +326,68 @@ def fixed_plan(codes, n_layers: int = 1):
             else:
                 o_src[t, layer] = t
                 cache_step = t
-            if c == WARS_REFRESH:
-                last_refresh = t
+            if c in (WARS_REFRESH, WARS_ASC_REFRESH):
+                last_refresh, half_r = t, c == WARS_ASC_REFRESH
     return code, r_src, o_src
 
 
 class LayerCache:
     """Per-layer state of the cache state machine: the residual of the latest
-    refresh (R) and the output of the latest non-AST step (O_cache)."""
+    refresh (R) and the output of the latest non-AST step (O_cache).
+
+    A WA-RS refresh keeps R for the whole batch; a WA-RS + ASC refresh keeps
+    it for the conditional half only (R then has B/2 entries), so a later
+    whole-batch WA-RS reuse has no residual for the unconditional half and is
+    rejected."""
 
     def __init__(self):
         self.R = None
         self.O_cache = None
 
 
-def plan_step(code: int, Q, K, V, cache: LayerCache, w: int) -> np.ndarray:
-    """One layer at one step under the plan (Sec. 3.2-3.4):
+def _residual_for(code: int, cache: LayerCache, B: int):
+    """The residual a reuse step reads (Sec. 3.2: that of the set's first step)."""
+    if cache.R is None:
+        raise ValueError("reuse before any refresh")
+    if code == WARS_REUSE:
+        if np.shape(cache.R)[0] != B:
+            raise ValueError("whole-batch reuse after a conditional-half (WA-RS + ASC) refresh")
+        return cache.R
+    return cache.R[: _cond_half(B)]  # WARS_ASC_REUSE: conditional entries
 
-      FULL     O = Attention                       R unchanged   O_cache <- O
-      REFRESH  O = Attention, R = O - W            R <- O - W    O_cache <- O
-      REUSE    O = W + R                           R unchanged   O_cache <- O
-      AST      O = O_cache                         R unchanged   O_cache unchanged
-      ASC      O[cond] = Attention, O[uncond] = O[cond]          O_cache <- O
+
+def plan_step(code: int, Q, K, V, cache: LayerCache, w: int) -> np.ndarray:
+    """One layer at one step under the plan (Sec. 3.2-3.5):
+
+      FULL              O = Attention                 R unchanged      O_cache <- O
+      REFRESH           O = Attention, R = O - W      R <- O - W       O_cache <- O
+      REUSE             O = W + R                     R unchanged      O_cache <- O
+      AST               O = O_cache                   R unchanged      O_cache unchanged
+      ASC               O[cond] = Attention, O[uncond] = O[cond]       O_cache <- O
+      WARS_ASC_REFRESH  REFRESH on the cond half, O[uncond] = O[cond]
+                                                      R <- cond-half R O_cache <- O
+      WARS_ASC_REUSE    REUSE on the cond half with R[cond], O[uncond] = O[cond]
+                                                      R unchanged      O_cache <- O
     """
+    B = np.shape(Q)[0] if Q is not None else None
     if code == FULL:
         O = attn_full(Q, K, V)
     elif code == WARS_REFRESH:
         O, R = wars_refresh(Q, K, V, w)
         cache.R = R
     elif code == WARS_REUSE:
-        if cache.R is None:
-            raise ValueError("reuse before any refresh")
-        O = wars_reuse(Q, K, V, cache.R, w)
+        O = wars_reuse(Q, K, V, _residual_for(code, cache, B), w)
     elif code == AST_REUSE:
         if cache.O_cache is None:
             raise ValueError("AST before any cached output")
         return ast_reuse(cache.O_cache)
     elif code == ASC_REUSE:
         O = asc_reuse(Q, K, V)
+    elif code == WARS_ASC_REFRESH:
+        O, R = wars_asc_refresh(Q, K, V, w)
+        cache.R = R
+    elif code == WARS_ASC_REUSE:
+        O = wars_asc_reuse(Q, K, V, _residual_for(code, cache, B), w)
     else:
         raise ValueError(f"unknown plan code {code}")
     cache.O_cache = O
@@ -345,26 +402,31 @@ def plan_step_rows(code: int, Q, K, V, rows, cache: LayerCache, w: int) -> np.nd
     head).  Attention rows are independent, so the per-row residual and output
     caches carried here equal the corresponding rows of the full ones."""
     rows = np.asarray(rows, dtype=np.int64)
+    B = np.shape(Q)[0] if Q is not None else None
+
+    def cond(x):
+        return np.asarray(x)[: _cond_half(B)]
+
     if code == FULL:
         O = attention_rows(Q, K, V, rows, None)
     elif code == WARS_REFRESH:
         O = attention_rows(Q, K, V, rows, None)
         cache.R = O - attention_rows(Q, K, V, rows, w)
     elif code == WARS_REUSE:
-        if cache.R is None:
-            raise ValueError("reuse before any refresh")
-        O = attention_rows(Q, K, V, rows, w) + cache.R
+        O = attention_rows(Q, K, V, rows, w) + _residual_for(code, cache, B)
     elif code == AST_REUSE:
         if cache.O_cache is None:
             raise ValueError("AST before any cached output")
         return cache.O_cache.copy()
     elif code == ASC_REUSE:
-        B = np.shape(Q)[0]
-        if B % 2:
-            raise ValueError("ASC needs an even batch")
-        half = B // 2
-        Oc = attention_rows(np.asarray(Q)[:half], np.asarray(K)[:half],
-                            np.asarray(V)[:half], rows, None)
+        Oc = attention_rows(cond(Q), cond(K), cond(V), rows, None)
+        O = np.concatenate([Oc, Oc], axis=0)
+    elif code == WARS_ASC_REFRESH:
+        Oc = attention_rows(cond(Q), cond(K), cond(V), rows, None)
+        cache.R = Oc - attention_rows(cond(Q), cond(K), cond(V), rows, w)
+        O = np.concatenate([Oc, Oc], axis=0)
+    elif code == WARS_ASC_REUSE:
+        Oc = attention_rows(cond(Q), cond(K), cond(V), rows, w) + _residual_for(code, cache, B)
         O = np.concatenate([Oc, Oc], axis=0)
     else:
         raise ValueError(f"unknown plan code {code}")

@@ -252,9 +252,64 @@ def check_plan_invariants(code, r_src, o_src, refresh_every):
                 last_refresh = t
 
 
+# P13 -- WA-RS + ASC (Sec. 3.5 strategy list, Table 2 row): the conditional
+# half is brute-force WA-RS on that half, the unconditional half a bitwise
+# copy; with identical halves (the guidance signal absent) it is WA-RS on the
+# whole batch; a reuse at unchanged inputs rebuilds the refresh output; the
+# residual kept is the conditional half's, and a whole-batch reuse after a
+# half-batch refresh is rejected.
+def pin_wars_asc():
+    B, H, L, d = 2, 1, 14, 8
+    Q, K, V = (_rand((B, H, L, d), s + 130) for s in (1, 2, 3))
+    for w in (0, 2, 13):
+        Oa, Rc = O.wars_asc_refresh(Q, K, V, w)
+        assert Oa.shape == (B, H, L, d) and Rc.shape == (1, H, L, d)
+        assert np.array_equal(Oa[:1], Oa[1:])
+        bf = O.brute_force_attention(Q[:1], K[:1], V[:1], None)
+        bw = O.brute_force_attention(Q[:1], K[:1], V[:1], w)
+        assert np.max(np.abs(Oa[:1] - bf)) <= 1e-12
+        assert np.max(np.abs(Rc - (bf - bw))) <= 1e-12
+        assert np.max(np.abs(O.wars_asc_reuse(Q, K, V, Rc, w)[1:] - bf)) <= 1e-12
+    assert not np.any(O.wars_asc_refresh(Q, K, V, L - 1)[1])
+    # identical halves: the combined strategy is plain WA-RS
+    B, H, L, d, w = 4, 2, 26, 16, 3
+    Qc, Kc, Vc = (_rand((B // 2, H, L, d), s + 140) for s in (1, 2, 3))
+    Q, K, V = (np.concatenate([x, x], axis=0) for x in (Qc, Kc, Vc))
+    Ow, Rw = O.wars_refresh(Q, K, V, w)
+    Oa, Rc = O.wars_asc_refresh(Q, K, V, w)
+    assert np.max(np.abs(Oa - Ow)) <= 1e-12 and np.max(np.abs(Rc - Rw[:B // 2])) <= 1e-12
+    # cache state machine: a full-batch refresh feeds a combined reuse with
+    # its conditional half; a combined refresh cannot feed a whole-batch reuse
+    Q, K, V = (_rand((B, H, L, d), s + 150) for s in (1, 2, 3))
+    Q2, K2, V2 = Q + 0.05 * _rand(Q.shape, 154), K + 0.05 * _rand(Q.shape, 155), V + 0.05 * _rand(Q.shape, 156)
+    cache = O.LayerCache()
+    O.plan_step(O.WARS_REFRESH, Q, K, V, cache, w)
+    R0 = cache.R.copy()
+    O1 = O.plan_step(O.WARS_ASC_REUSE, Q2, K2, V2, cache, w)
+    ref = O.attn_window(Q2[:B // 2], K2[:B // 2], V2[:B // 2], w) + R0[:B // 2]
+    assert np.max(np.abs(O1[:B // 2] - ref)) <= 1e-15 and np.array_equal(O1[B // 2:], O1[:B // 2])
+    assert np.array_equal(cache.R, R0) and np.array_equal(cache.O_cache, O1)
+    O2 = O.plan_step(O.WARS_ASC_REFRESH, Q, K, V, cache, w)
+    assert cache.R.shape[0] == B // 2 and np.array_equal(cache.O_cache, O2)
+    assert np.max(np.abs(O2[:B // 2] - O.attn_full(Q[:B // 2], K[:B // 2], V[:B // 2]))) <= 1e-15
+    # at B = 2 a one-entry residual would broadcast silently over the batch
+    Q, K, V = Q[:2], K[:2], V[:2]
+    cache = O.LayerCache()
+    O.plan_step(O.WARS_ASC_REFRESH, Q, K, V, cache, w)
+    try:
+        O.plan_step(O.WARS_REUSE, Q, K, V, cache, w)
+    except ValueError:
+        pass
+    else:
+        raise AssertionError("whole-batch reuse after a half-batch refresh must be rejected")
+    code, r_src, o_src = O.fixed_plan([O.WARS_REFRESH, O.WARS_ASC_REUSE, O.WARS_ASC_REFRESH, O.AST_REUSE,
+                                       O.WARS_ASC_REUSE])
+    assert r_src[:, 0].tolist() == [-1, 0, -1, -1, 2] and o_src[:, 0].tolist() == [0, 1, 2, 2, 4]
+
+
 ALL_PINS = {
     "P1": pin_brute_force, "P2": pin_torch_sdpa, "P3": pin_wide_band, "P4": pin_zero_band,
     "P5": pin_zero_query, "P6": pin_constant_values, "P7": pin_probabilities,
     "P8": pin_refresh_reuse_algebra, "P9": pin_sharing, "P10": pin_permutation,
-    "P11": pin_table2, "P12": pin_plan,
+    "P11": pin_table2, "P12": pin_plan, "P13": pin_wars_asc,
 }

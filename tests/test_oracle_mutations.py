@@ -11,7 +11,7 @@ from oracle import dfa_oracle as O
 from tests import oracle_pins as pins
 
 # cheap pins first: a mutation stops at the first pin that catches it
-ORDER = ["P4", "P3", "P6", "P7", "P5", "P8", "P9", "P10", "P12", "P2", "P1", "P11"]
+ORDER = ["P4", "P3", "P6", "P7", "P5", "P8", "P9", "P10", "P12", "P13", "P2", "P1", "P11"]
 
 
 def _probs_factory(scale_fn=None, transpose=False, axis=-1):
@@ -68,6 +68,30 @@ def _asc_uncond_source(Q, K, V):
     half = np.shape(Q)[0] // 2
     Ou = O.attn_full(np.asarray(Q)[half:], np.asarray(K)[half:], np.asarray(V)[half:])
     return np.concatenate([Ou, Ou], axis=0)
+
+
+def _wars_asc_uncond_source(Q, K, V, w):
+    half = np.shape(Q)[0] // 2
+    Ou, Ru = O.wars_refresh(np.asarray(Q)[half:], np.asarray(K)[half:], np.asarray(V)[half:], w)
+    return np.concatenate([Ou, Ou], axis=0), Ru
+
+
+def _wars_asc_reuse_no_residual(Q, K, V, R_cond, w):
+    half = np.shape(Q)[0] // 2
+    Oc = O.attn_window(np.asarray(Q)[:half], np.asarray(K)[:half], np.asarray(V)[:half], w)
+    return np.concatenate([Oc, Oc], axis=0)
+
+
+def _residual_wrong_half(code, cache, B):
+    if cache.R is None:
+        raise ValueError("reuse before any refresh")
+    return cache.R if code == O.WARS_REUSE else cache.R[-(B // 2):]
+
+
+def _residual_unchecked(code, cache, B):
+    if cache.R is None:
+        raise ValueError("reuse before any refresh")
+    return cache.R if code == O.WARS_REUSE else cache.R[: B // 2]
 
 
 _orig_plan_step = O.plan_step
@@ -139,6 +163,10 @@ MUTATIONS = {
     "residual_sign": ("wars_refresh", _refresh_sign),
     "reuse_adds_to_full": ("wars_reuse", _reuse_on_full),
     "asc_wrong_half": ("asc_reuse", _asc_uncond_source),
+    "wars_asc_wrong_half": ("wars_asc_refresh", _wars_asc_uncond_source),
+    "wars_asc_reuse_drops_residual": ("wars_asc_reuse", _wars_asc_reuse_no_residual),
+    "wars_asc_reads_uncond_residual": ("_residual_for", _residual_wrong_half),
+    "half_residual_feeds_full_reuse": ("_residual_for", _residual_unchecked),
     "full_clears_residual": ("plan_step", _plan_step_full_clears_R),
     "splitmix_shift_typo": ("SplitMix64", _SplitMixTypo),
     "refresh_age_off_by_one": ("plan_make", _plan_age_off_by_one),
