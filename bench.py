@@ -10,7 +10,9 @@ resident in HBM before the timed region.
 
 Printed: one JSON line.  `value` is the executed algorithmic attention
 throughput of the plan run (FULL/REFRESH 4*B*H*L^2*d, REUSE 4*B*H*d*N_band,
-ASC 2*B*H*L^2*d, AST 0 FLOPs per layer-step) in TFLOP/s.  Also reported:
+ASC 2*B*H*L^2*d, AST 0 FLOPs per layer-step) in TFLOP/s.  The combined
+WA-RS + ASC codes are not drawn by the seeded plan; their kernels are timed
+on their own next to the others.  Also reported:
 ms per layer-step of the plan run and of a full-attention-only run on the
 same inputs, per-kernel times, the roofline of the dominant kernel (the full
 attention kernel, measured with HIP events on its launch stream inside the
@@ -63,7 +65,8 @@ def n_band(L: int, w: int) -> int:
 
 def code_flops(code: int, B: int, H: int, L: int, d: int, w: int) -> float:
     full = 4.0 * B * H * L * L * d
-    return {0: full, 1: full, 2: 4.0 * B * H * d * n_band(L, w), 3: 0.0, 4: full / 2}[code]
+    band = 4.0 * B * H * d * n_band(L, w)
+    return {0: full, 1: full, 2: band, 3: 0.0, 4: full / 2, 5: full / 2, 6: band / 2}[code]
 
 
 def parse():
@@ -207,6 +210,10 @@ def main():
         "asc": (lambda: dfa.dfa_plan_step(dfa.ASC_REUSE, q, k, v, Ok, None, None, w, stream),
                 code_flops(4, B, H, L, d, w), 2.5),
         "ast_copy": (lambda: dfa.dfa_plan_step(dfa.AST_REUSE, None, None, None, Ok, None, Ck, w, stream), 0.0, 2),
+        "wars_asc_refresh": (lambda: dfa.dfa_plan_step(dfa.WARS_ASC_REFRESH, q, k, v, Ok, Rk, None, w, stream),
+                             code_flops(5, B, H, L, d, w), 3.5),
+        "wars_asc_reuse": (lambda: dfa.dfa_plan_step(dfa.WARS_ASC_REUSE, q, k, v, Ok, Rk, None, w, stream),
+                           code_flops(6, B, H, L, d, w), 3.5),
     }
     tensor_bytes = B * H * L * d * 2
     kres = {}
@@ -251,6 +258,12 @@ def main():
         },
         "plan_speedup_vs_full_only": round(full_only_ms / ms_per_step, 3),
         "plan_code_counts": {dfa.CODE_NAMES[c].lower(): int((code == c).sum()) for c in range(5)},
+        # kernel time of each strategy's compressed step relative to full
+        # attention at the same shape (the latency rows of Table 2)
+        "latency_fraction_vs_full": {
+            name: round(kres[key]["ms"] / kres["full"]["ms"], 4)
+            for name, key in (("asc", "asc"), ("wars", "wars_reuse"), ("wars_asc", "wars_asc_reuse"),
+                              ("ast", "ast_copy"))},
         "full_equiv_tflops": round(plan_layer_steps * full_flops / (ms_per_step * 1e-3) / 1e12, 1),
         "kernels": kres,
         "reuse_speedup_vs_full": round(kres["full"]["ms"] / kres["wars_reuse"]["ms"], 3),

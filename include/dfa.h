@@ -70,7 +70,9 @@ enum {
     DFA_WARS_REFRESH = 1,  /* WA-RS, first step of a set: O = Attn, R = O - W  (Eq. 1) */
     DFA_WARS_REUSE = 2,    /* WA-RS, later step:          O = W + R            (Eq. 2) */
     DFA_AST_REUSE = 3,     /* AST: O = the layer's cached output (Sec. 3.3)    */
-    DFA_ASC_REUSE = 4      /* ASC: conditional half computed, copied to the unconditional half (Sec. 3.4) */
+    DFA_ASC_REUSE = 4,     /* ASC: conditional half computed, copied to the unconditional half (Sec. 3.4) */
+    DFA_WARS_ASC_REFRESH = 5,  /* WA-RS + ASC: REFRESH on the conditional half, output copied */
+    DFA_WARS_ASC_REUSE = 6     /* WA-RS + ASC: REUSE on the conditional half, output copied   */
 };
 
 /* Full self-attention (Sec. 3.2, first line of Eq. 1):
@@ -101,8 +103,10 @@ dfa_status dfa_attn_window_plus_residual(const void* Q, const void* K, const voi
 
 /* One plan entry of one layer at one step: dispatches `code` and maintains the
  * caller's per-layer caches.
- *   R       the layer's fp32 residual buffer [B,H,L,d]: written by DFA_WARS_REFRESH,
- *           read by DFA_WARS_REUSE (required for both; ignored otherwise).
+ *   R       the layer's fp32 residual buffer [B,H,L,d]: written by the two
+ *           REFRESH codes, read by the two REUSE codes (required for all four;
+ *           ignored otherwise).  The WA-RS + ASC codes touch only its first
+ *           B/2 entries (the conditional half).
  *   Ocache  the layer's output cache [B,H,L,d] for AST (Sec. 3.3).  Every
  *           computed step (all codes except AST) also writes its output here,
  *           and DFA_AST_REUSE copies it to O.  Ocache == O makes AST a no-op
@@ -114,10 +118,20 @@ dfa_status dfa_attn_window_plus_residual(const void* Q, const void* K, const voi
  *           AST       O = Ocache
  *           ASC       O[b] = O[b+B/2] = Attention on the conditional entry b
  *                     (b < B/2; B must be even)
+ *           WARS_ASC_REFRESH   (WA-RS and ASC together, the strategy list of
+ *                     Sec. 3.5 and Table 2)  for b < B/2:
+ *                     O[b] = O[b+B/2] = Attention, R[b] = O[b] - W[b];
+ *                     R[b+B/2] is left untouched
+ *           WARS_ASC_REUSE     for b < B/2: O[b] = O[b+B/2] = W[b] + R[b]
+ * A WARS_ASC_REUSE may follow either refresh code (it reads only R's
+ * conditional half).  A whole-batch WARS_REUSE must follow a whole-batch
+ * WARS_REFRESH: after a WARS_ASC_REFRESH the unconditional half of R is stale,
+ * and the library, which keeps no state, cannot detect that misuse.
  * The ASC copy and the cache write are fused into the attention kernel's
  * store (each output tile is written to every destination), not separate
- * passes.  Returns DFA_ERR_INVALID_ARG for an unknown code, odd B with ASC,
- * a missing R or Ocache, or overlapping outputs. */
+ * passes.  Returns DFA_ERR_INVALID_ARG for an unknown code, odd B with a
+ * half-batch code (ASC, WARS_ASC_*), a missing R or Ocache, or overlapping
+ * outputs. */
 dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, void* O, void* R,
                          void* Ocache, int B, int H, int L, int d, int w, hipStream_t stream);
 

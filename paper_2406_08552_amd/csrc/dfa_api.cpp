@@ -182,7 +182,7 @@ dfa_status dfa_attn_window_plus_residual(const void* Q, const void* K, const voi
 
 dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, void* O, void* R, void* Ocache,
                          int B, int H, int L, int d, int w, hipStream_t stream) {
-    if (code < DFA_FULL || code > DFA_ASC_REUSE) return fail(DFA_ERR_INVALID_ARG, "unknown plan code %d", code);
+    if (code < DFA_FULL || code > DFA_WARS_ASC_REUSE) return fail(DFA_ERR_INVALID_ARG, "unknown plan code %d", code);
     Shape s;
     dfa_status st;
     if ((st = check_shape(B, H, L, d, w, &s)) != DFA_OK) return st;
@@ -198,9 +198,12 @@ dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, 
         return hip_status(dfa::launch_copy(Ocache, O, s.bytes, stream), "AST copy launch");
     }
 
+    const bool half_batch = code == DFA_ASC_REUSE || code == DFA_WARS_ASC_REFRESH || code == DFA_WARS_ASC_REUSE;
+    if (half_batch && (B % 2)) return fail(DFA_ERR_INVALID_ARG, "plan code %d needs an even batch (B=%d)", code, B);
     if ((st = check_qkv(Q, K, V)) != DFA_OK) return st;
     if ((st = check_out_vs_inputs(O, "O", Q, K, V, s.bytes)) != DFA_OK) return st;
-    const bool uses_r = code == DFA_WARS_REFRESH || code == DFA_WARS_REUSE;
+    const bool uses_r = code == DFA_WARS_REFRESH || code == DFA_WARS_REUSE || code == DFA_WARS_ASC_REFRESH ||
+                        code == DFA_WARS_ASC_REUSE;
     if (uses_r) {
         if ((st = check_ptr(R, "R")) != DFA_OK) return st;
         if ((st = check_out_vs_inputs(R, "R", Q, K, V, s.bytes, s.rbytes)) != DFA_OK) return st;
@@ -211,10 +214,10 @@ dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, 
     dfa::AttnLaunch a = make_launch(Q, K, V, s);
     a.dst[0] = O;
     a.ndst = 1;
-    if (code == DFA_ASC_REUSE) {
-        if (B % 2) return fail(DFA_ERR_INVALID_ARG, "ASC needs an even batch (B=%d)", B);
-        // attention on the conditional half; every output tile is also stored
-        // at its unconditional partner (and in the cache)
+    if (half_batch) {
+        // attention on the conditional half (entries 0..B/2-1, which are also
+        // the first half of R); every output tile is also stored at its
+        // unconditional partner (and in the cache)
         const size_t half = s.bytes / 2;
         a.B = B / 2;
         a.dst[a.ndst++] = (char*)O + half;
@@ -222,16 +225,19 @@ dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, 
             a.dst[a.ndst++] = Ocache;
             a.dst[a.ndst++] = (char*)Ocache + half;
         }
-        return hip_status(dfa::launch_asc(a, stream), "ASC launch");
+    } else if (sep) {
+        a.dst[a.ndst++] = Ocache;
     }
-    if (sep) a.dst[a.ndst++] = Ocache;
     switch (code) {
         case DFA_FULL:
             return hip_status(dfa::launch_full(a, stream), "FULL launch");
+        case DFA_ASC_REUSE:
+            return hip_status(dfa::launch_asc(a, stream), "ASC launch");
         case DFA_WARS_REFRESH:
+        case DFA_WARS_ASC_REFRESH:
             a.Rout = R;
             return hip_status(dfa::launch_refresh(a, stream), "WA-RS refresh launch");
-        default:  // DFA_WARS_REUSE
+        default:  // DFA_WARS_REUSE, DFA_WARS_ASC_REUSE
             a.Rin = R;
             return hip_status(dfa::launch_window(a, stream), "WA-RS reuse launch");
     }

@@ -22,8 +22,10 @@ from .build import LIB_PATH
 
 DFA_OK, DFA_ERR_INVALID_ARG, DFA_ERR_UNSUPPORTED, DFA_ERR_HIP = 0, 1, 2, 3
 FULL, WARS_REFRESH, WARS_REUSE, AST_REUSE, ASC_REUSE = 0, 1, 2, 3, 4
+WARS_ASC_REFRESH, WARS_ASC_REUSE = 5, 6
 CODE_NAMES = {FULL: "FULL", WARS_REFRESH: "WARS_REFRESH", WARS_REUSE: "WARS_REUSE",
-              AST_REUSE: "AST_REUSE", ASC_REUSE: "ASC_REUSE"}
+              AST_REUSE: "AST_REUSE", ASC_REUSE: "ASC_REUSE",
+              WARS_ASC_REFRESH: "WARS_ASC_REFRESH", WARS_ASC_REUSE: "WARS_ASC_REUSE"}
 
 # every symbol include/dfa.h declares
 EXPORTS = ("dfa_attn_full", "dfa_attn_full_and_residual", "dfa_attn_window_plus_residual",

@@ -89,8 +89,13 @@ def test_plan_step_validation(L):
     assert "Ocache" in dfa.last_error()
     # AST with the cache equal to O is a no-op: OK without any device work
     assert f(dfa.AST_REUSE, None, None, None, D_, None, D_, *args) == dfa.DFA_OK
-    assert f(dfa.ASC_REUSE, A, B_, C_, D_, None, None, 3, 2, 64, 72, 8, None) == dfa.DFA_ERR_INVALID_ARG
-    assert "even" in dfa.last_error()
+    for code in (dfa.ASC_REUSE, dfa.WARS_ASC_REFRESH, dfa.WARS_ASC_REUSE):
+        assert f(code, A, B_, C_, D_, E_, None, 3, 2, 64, 72, 8, None) == dfa.DFA_ERR_INVALID_ARG
+        assert "even" in dfa.last_error()
+    for code in (dfa.WARS_ASC_REFRESH, dfa.WARS_ASC_REUSE):
+        assert f(code, A, B_, C_, D_, None, None, *args) == dfa.DFA_ERR_INVALID_ARG   # R missing
+        assert "R is NULL" in dfa.last_error()
+        assert f(code, A, B_, C_, D_, D_, None, *args) == dfa.DFA_ERR_INVALID_ARG     # O == R
     assert f(dfa.FULL, A, B_, C_, D_, None, D_ + 32, *args) == dfa.DFA_ERR_INVALID_ARG  # cache overlaps O
     assert f(dfa.FULL, A, B_, C_, D_, None, A, *args) == dfa.DFA_ERR_INVALID_ARG       # cache aliases Q
     assert f(dfa.FULL, None, B_, C_, D_, None, None, *args) == dfa.DFA_ERR_INVALID_ARG

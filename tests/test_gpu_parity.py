@@ -187,21 +187,34 @@ def test_tiny_three_step_check():
             say(f"tiny step 0 vs fp32 masters: max abs {e32:.3e}")
 
 
-def run_plan(cfg_key, layers, n_steps, n_rows=None, alias_cache=()):
+HALF_BATCH = (dfa.ASC_REUSE, dfa.WARS_ASC_REFRESH, dfa.WARS_ASC_REUSE)
+# a legal sequence that runs every plan code, including a combined reuse fed
+# by a whole-batch refresh and one fed by a conditional-half refresh
+MIXED_CODES = [dfa.WARS_REFRESH, dfa.WARS_REUSE, dfa.WARS_ASC_REUSE, dfa.AST_REUSE, dfa.WARS_ASC_REFRESH,
+               dfa.WARS_ASC_REUSE, dfa.ASC_REUSE, dfa.FULL, dfa.AST_REUSE, dfa.WARS_REFRESH, dfa.WARS_REUSE,
+               dfa.WARS_ASC_REUSE]
+
+
+def run_plan(cfg_key, layers, n_steps, n_rows=None, alias_cache=(), codes=None):
     cfg = inputs.CONFIGS[cfg_key]
     dev = torch.device("cuda")
     shape = (cfg.B, cfg.H, cfg.L, cfg.d)
-    code, r_src, o_src = dfa.dfa_plan_make(cfg.plan_seed, cfg.n_layers, cfg.n_steps, cfg.refresh_every, cfg.B)
-    ref_plan = orc.plan_make(cfg.plan_seed, cfg.n_layers, cfg.n_steps, cfg.refresh_every, cfg.B)
-    for a, b in zip((code, r_src, o_src), ref_plan):
-        assert np.array_equal(a, b)
+    half = cfg.B // 2
+    if codes is None:
+        code, r_src, o_src = dfa.dfa_plan_make(cfg.plan_seed, cfg.n_layers, cfg.n_steps, cfg.refresh_every, cfg.B)
+        ref_plan = orc.plan_make(cfg.plan_seed, cfg.n_layers, cfg.n_steps, cfg.refresh_every, cfg.B)
+        for a, b in zip((code, r_src, o_src), ref_plan):
+            assert np.array_equal(a, b)
+    else:
+        code, r_src, o_src = orc.fixed_plan(codes, n_layers=max(layers) + 1)
     rows = None if n_rows is None else inputs.sample_rows(cfg.L, n_rows, cfg.cfg_id)
     seen = set()
     for layer in layers:
         gen = inputs.DriftingQKV(cfg.cfg_id, layer, shape, cfg.drift)
-        O = torch.empty(shape, dtype=torch.bfloat16, device=dev)
-        R = torch.empty(shape, dtype=torch.float32, device=dev)
-        Oc = O if layer in alias_cache else torch.empty_like(O)
+        O = Guarded(shape, dev).t
+        Rg = Guarded(shape, dev, torch.float32)
+        R = Rg.t
+        Oc = O if layer in alias_cache else Guarded(shape, dev).t
         cache = orc.LayerCache()
         outputs = {}
         for t in range(n_steps):
@@ -209,6 +222,8 @@ def run_plan(cfg_key, layers, n_steps, n_rows=None, alias_cache=()):
             c = int(code[t, layer])
             seen.add(c)
             say(f"{cfg_key} layer {layer} step {t} code {dfa.CODE_NAMES[c]}")
+            if t == 0:
+                R_before = R.cpu()
             if c == dfa.AST_REUSE:
                 dfa.dfa_plan_step(c, None, None, None, O, R, Oc, cfg.w)
             else:
@@ -223,13 +238,18 @@ def run_plan(cfg_key, layers, n_steps, n_rows=None, alias_cache=()):
             check(f"{cfg_key} l{layer} t{t} O", got, ref, rows)
             if c == dfa.WARS_REFRESH:
                 check(f"{cfg_key} l{layer} t{t} R", R, cache.R, rows)
+            if c == dfa.WARS_ASC_REFRESH:
+                check(f"{cfg_key} l{layer} t{t} R[cond]", R[:half], cache.R, rows)
+                assert torch.equal(R[half:].cpu(), R_before[half:]), "a half-batch refresh must leave R[uncond]"
             if c == dfa.AST_REUSE:
                 assert torch.equal(got, outputs[int(o_src[t, layer])]), "AST must return the cached step bitwise"
             else:
                 outputs[t] = got
                 assert torch.equal(Oc.cpu(), got), "computed steps must refresh the cache"
-            if c == dfa.ASC_REUSE:
-                assert torch.equal(got[: cfg.B // 2], got[cfg.B // 2:]), "ASC halves must be bit-identical"
+            if c in HALF_BATCH:
+                assert torch.equal(got[:half], got[half:]), "CFG-shared halves must be bit-identical"
+            R_before = R.cpu()
+        assert Rg.guards_intact(), "write outside R"
     return seen
 
 
@@ -249,3 +269,81 @@ def test_plan_pixart1k_sampled():
 def test_plan_pixart2k_sampled():
     seen = run_plan("pixart2k", layers=[2], n_steps=9, n_rows=64)
     assert dfa.WARS_REFRESH in seen
+
+
+def test_plan_mixed_codes_dit256():
+    """Every plan code, including WA-RS + ASC after both kinds of refresh."""
+    seen = run_plan("dit256", layers=[0, 1], n_steps=len(MIXED_CODES), alias_cache={1}, codes=MIXED_CODES)
+    assert seen == set(dfa.CODE_NAMES)
+
+
+def test_plan_mixed_codes_pixart2k_sampled():
+    run_plan("pixart2k", layers=[4], n_steps=len(MIXED_CODES), n_rows=48, codes=MIXED_CODES)
+
+
+def test_wars_asc_odd_shapes():
+    """WA-RS + ASC on ragged tiles and degenerate bands (B = 4: two CFG pairs)."""
+    dev = torch.device("cuda")
+    for (B, H, L, d, w) in ((4, 1, 77, 72, 5), (2, 2, 129, 64, 0), (4, 2, 300, 72, 299), (2, 1, 1, 72, 0)):
+        shape = (B, H, L, d)
+        say(f"wars+asc B={B} H={H} L={L} d={d} w={w}")
+        q0, k0, v0 = rand_qkv(shape, 300 + L + w)
+        q1, k1, v1 = (x + 0.05 * y for x, y in zip((q0, k0, v0), rand_qkv(shape, 400 + L)))
+        O, Oc = Guarded(shape, dev), Guarded(shape, dev)
+        Rg = Guarded(shape, dev, torch.float32)
+        Rg.t.fill_(-7.0)
+        cache = orc.LayerCache()
+        for c, (q, k, v) in ((dfa.WARS_ASC_REFRESH, (q0, k0, v0)), (dfa.WARS_ASC_REUSE, (q1, k1, v1))):
+            dfa.dfa_plan_step(c, q.to(dev), k.to(dev), v.to(dev), O.t, Rg.t, Oc.t, w)
+            torch.cuda.synchronize()
+            ref = orc.plan_step(c, f64(q), f64(k), f64(v), cache, w)
+            check(f"wars+asc {dfa.CODE_NAMES[c]} O", O.t, ref)
+            got = O.t.cpu()
+            assert torch.equal(got[: B // 2], got[B // 2:]) and torch.equal(Oc.t.cpu(), got)
+        check("wars+asc R[cond]", Rg.t[: B // 2], cache.R)
+        assert bool(torch.all(Rg.t[B // 2:] == -7.0)), "R[uncond] must stay untouched"
+        if w >= L - 1:
+            assert not torch.any(Rg.t[: B // 2] != 0), "w >= L-1 must give R == 0 exactly"
+        for g in (O, Oc, Rg):
+            assert g.guards_intact(), "write outside an output tensor"
+
+
+def test_checkpoint_resume_bit_exact():
+    """Stop a plan run after step k, move the layer's caches (R, Ocache) to the
+    host and back into fresh buffers, continue: every later output equals the
+    uninterrupted run bit for bit."""
+    cfg = inputs.CONFIGS["dit256"]
+    dev = torch.device("cuda")
+    shape = (cfg.B, cfg.H, cfg.L, cfg.d)
+    steps = [inputs.bf16_qkv(cfg.cfg_id, 0, t, shape) for t in range(len(MIXED_CODES))]
+    steps = [tuple(x.to(dev) for x in qkv) for qkv in steps]
+
+    def fresh():
+        return (torch.zeros(shape, dtype=torch.bfloat16, device=dev),
+                torch.zeros(shape, dtype=torch.float32, device=dev),
+                torch.zeros(shape, dtype=torch.bfloat16, device=dev))
+
+    def run(t0, t1, O, R, Oc):
+        outs = []
+        for t in range(t0, t1):
+            c = MIXED_CODES[t]
+            q, k, v = steps[t] if c != dfa.AST_REUSE else (None, None, None)
+            dfa.dfa_plan_step(c, q, k, v, O, R, Oc, cfg.w)
+            outs.append(O.clone())
+        torch.cuda.synchronize()
+        return outs
+
+    say("checkpoint/resume: uninterrupted run")
+    ref = run(0, len(MIXED_CODES), *fresh())
+    for k in (3, 5, 9):
+        say(f"checkpoint/resume: cut after step {k - 1}")
+        O, R, Oc = fresh()
+        run(0, k, O, R, Oc)
+        saved = (R.cpu(), Oc.cpu())
+        del O, R, Oc
+        O2, R2, Oc2 = fresh()
+        R2.copy_(saved[0])
+        Oc2.copy_(saved[1])
+        outs = run(k, len(MIXED_CODES), O2, R2, Oc2)
+        for t, got in zip(range(k, len(MIXED_CODES)), outs):
+            assert torch.equal(got, ref[t]), f"resumed run differs at step {t} ({dfa.CODE_NAMES[MIXED_CODES[t]]})"
