@@ -11,8 +11,8 @@
 //   (batch, head); each wavefront owns 32 of them (two 16-query MFMA blocks).
 //   The workgroup walks key tiles of BK = 64 keys, staged in LDS with double
 //   buffering (global loads of the next tile are in flight while the current
-//   one is used).  Two workgroups share a CU (two wavefronts per SIMD), so the
-//   MFMA work of one overlaps the softmax arithmetic of the other.
+//   one is used).  Three workgroups share a CU (three wavefronts per SIMD), so
+//   the MFMA work of one overlaps the softmax arithmetic of the others.
 //
 // MFMA mapping (v_mfma_f32_16x16x32_bf16, fp32 accumulation)
 //   Scores are formed transposed, S^T = K Q^T: A = 16 keys x 32 dims from LDS,
@@ -34,7 +34,9 @@
 //   Per query a running max m (log2 domain) and accumulator (O, l).  The max
 //   is updated lazily: the accumulator is rescaled only when a tile's max
 //   exceeds m by more than 8 (so probabilities stay below 2^8 and the
-//   rescale is almost never taken after the first tiles).
+//   rescale is almost never taken after the first tiles).  Each lane tests
+//   its own scores against that threshold; the exact maxima across lanes are
+//   formed only inside the rare rescale branch.
 //
 // Tile walk and band handling
 //   The key tiles a workgroup visits are split into segments so that the hot
@@ -183,7 +185,9 @@ struct Tile {
 template <int D>
 struct Acc {
     f32x4 o[QBW][Geo<D>::NDB];   // O^T: lane holds dims 16*m + 4*g + i of query lane%16
-    float m[QBW];                // running max, log2 domain (NEG_INF = none yet)
+    // The running max m (log2 domain) is kept in two derived forms:
+    float negm[QBW];             // -m, or 0 while the query has seen no finite score
+    float thr[QBW];              // (m + RESCALE_THRESH) / c in raw score units (-inf: no m yet)
     float l[QBW];                // lane-partial row sum (unused when a ones row is present)
 
     __device__ __forceinline__ void init() {
@@ -191,7 +195,8 @@ struct Acc {
         for (int qb = 0; qb < QBW; ++qb) {
 #pragma unroll
             for (int mb = 0; mb < Geo<D>::NDB; ++mb) o[qb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            m[qb] = NEG_INF;
+            negm[qb] = 0.f;
+            thr[qb] = NEG_INF;
             l[qb] = 0.f;
         }
     }
@@ -215,10 +220,11 @@ __device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, cons
         bf16x8 ka[G::NC32 > 0 ? G::NC32 : 1];
 #pragma unroll
         for (int c = 0; c < G::NC32; ++c) ka[c] = as_bf16x8(*(const u32x4*)(krow + 32 * c + 8 * g));
+        // tail dims: lane rows g >= TAIL/8 re-read the row's first tail chunk;
+        // their Q tail fragment is zero, so those products vanish (the values
+        // read belong to the same key row, so no other row's data enters)
         u32x4 kt = u32x4{0u, 0u, 0u, 0u};
-        if constexpr (G::TAIL > 0) {
-            if (8 * g < G::TAIL) kt = *(const u32x4*)(krow + G::D32 + 8 * g);
-        }
+        if constexpr (G::TAIL > 0) kt = *(const u32x4*)(krow + G::D32 + (8 * g < G::TAIL ? 8 * g : 0));
 #pragma unroll
         for (int qb = 0; qb < QBW; ++qb) {
             f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -255,37 +261,43 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
             }
         }
     }
-    // tile max per query, and the lazy rescale (one branch for both blocks)
-    float mx[QBW];
-    bool need[QBW];
-    bool need_any = false;
+    // Lazy rescale.  Each lane compares the largest of its own scores with
+    // its query's threshold (m + RESCALE_THRESH) / c; only when some lane of
+    // the wavefront exceeds it (one wave-uniform branch, rarely taken after
+    // the first tiles) are the exact tile maxima formed over the four lanes
+    // that share a query, and the queries whose maximum grew by more than
+    // the margin are rescaled.  Otherwise every probability is below 2^8.
+    float v[QBW];
+    bool hot = false;
 #pragma unroll
     for (int qb = 0; qb < QBW; ++qb) {
-        float v = NEG_INF;
+        v[qb] = NEG_INF;
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) v = fmaxf(v, S.s[qb][kb][i]);
-        mx[qb] = group_max(v) * c;
-        need[qb] = mx[qb] > acc.m[qb] + RESCALE_THRESH;
-        need_any = need_any || need[qb];
+            for (int i = 0; i < 4; ++i) v[qb] = fmaxf(v[qb], S.s[qb][kb][i]);
+        hot = hot || v[qb] > acc.thr[qb];
     }
-    if (__any(need_any)) {
+    if (__any(hot)) {
 #pragma unroll
         for (int qb = 0; qb < QBW; ++qb) {
-            const float mnew = need[qb] ? mx[qb] : acc.m[qb];
-            const float alpha = need[qb] ? __builtin_amdgcn_exp2f(acc.m[qb] - mnew) : 1.0f;
+            const float mx = group_max(v[qb]) * c;
+            const float m = acc.thr[qb] == NEG_INF ? NEG_INF : -acc.negm[qb];
+            if (mx > m + RESCALE_THRESH) {
+                const float alpha = __builtin_amdgcn_exp2f(m - mx);
 #pragma unroll
-            for (int mb = 0; mb < G::NDB; ++mb) acc.o[qb][mb] *= alpha;
-            acc.l[qb] *= alpha;
-            acc.m[qb] = mnew;
+                for (int mb = 0; mb < G::NDB; ++mb) acc.o[qb][mb] *= alpha;
+                acc.l[qb] *= alpha;
+                acc.negm[qb] = -mx;
+                acc.thr[qb] = (mx + RESCALE_THRESH) / c;
+            }
         }
     }
     // probabilities, packed to bf16 as the B operand of PV
     bf16x8 pb[QBW][BK / 32];
 #pragma unroll
     for (int qb = 0; qb < QBW; ++qb) {
-        const float mbase = acc.m[qb] == NEG_INF ? 0.0f : acc.m[qb];
+        const float negm = acc.negm[qb];
         float psum = 0.f;
 #pragma unroll
         for (int h = 0; h < BK / 32; ++h) {
@@ -293,10 +305,10 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
                 const f32x4 s = S.s[qb][2 * h + half];
-                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0], c, -mbase));
-                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1], c, -mbase));
-                const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2], c, -mbase));
-                const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[3], c, -mbase));
+                const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[0], c, negm));
+                const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1], c, negm));
+                const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2], c, negm));
+                const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[3], c, negm));
                 if constexpr (!G::ONES) psum += (p0 + p1) + (p2 + p3);
                 wds[2 * half + 0] = pack_bf16x2(p0, p1);
                 wds[2 * half + 1] = pack_bf16x2(p2, p3);
@@ -617,8 +629,8 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     }
 }
 
-// Two waves per SIMD (register budget 256): the MFMA work of one wavefront
-// overlaps the softmax arithmetic of the other.
+// Three waves per SIMD (register budget 168): the MFMA work of one wavefront
+// overlaps the softmax arithmetic of the others.
 template <int D, int MODE>
 __global__ void __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(3, 3))) attn_kernel(Params p) {
     __shared__ __attribute__((aligned(16))) uint16_t smem[2 * Geo<D>::STAGE_ELEMS];
@@ -662,7 +674,7 @@ hipError_t launch_attn(const AttnLaunch& a, hipStream_t stream) {
     if (nb <= 0 || nb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
     p.nblocks = (int)nb;
     p.c = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-    static_assert((size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t) <= 80 * 1024, "two workgroups per CU must fit in LDS");
+    static_assert((size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t) * 3 <= 160 * 1024, "three workgroups per CU must fit in LDS");
     hipLaunchKernelGGL((attn_kernel<D, MODE>), dim3(p.nblocks), dim3(NTHREADS), 0, stream, p);
     return hipGetLastError();
 }
