@@ -21,6 +21,8 @@ the paper's order and notation (DiTFastAttn, arXiv 2406.08552):
                                  SplitMix64 stream instead of searched
   * attention-FLOP accounting -- Table 2 ("Attn FLOPs" of the multi-head attention
                                  module, window = 1/8 of the tokens, Sec. 4.1)
+  * the attention module      -- QKV projection, attention under the plan, output
+                                 projection; AST/ASC skip or halve the whole module
 
 Readings of points the paper leaves open (all listed with reasons in the
 design notes):
@@ -432,6 +434,86 @@ def plan_step_rows(code: int, Q, K, V, rows, cache: LayerCache, w: int) -> np.nd
         raise ValueError(f"unknown plan code {code}")
     cache.O_cache = O
     return O
+
+
+# ---------------------------------------------------------------------------
+# The attention module around the path (Sec. 3.1; the module of Table 2's
+# "Attn FLOPs"): a fused QKV projection, multi-head attention, an output
+# projection.  Layout: X [B, L, C] with C = H * d; the projection's output
+# features are ordered (q | k | v), each H heads of d dims; weights use the
+# [out_features, in_features] convention (y = x W^T + b).
+# ---------------------------------------------------------------------------
+def qkv_proj(X, Wqkv, bqkv, H: int):
+    """Q, K, V [B, H, L, d] = split(X W_qkv^T + b_qkv)."""
+    X = np.asarray(X, dtype=np.float64)
+    B, L, C = X.shape
+    d = C // H
+    Y = X @ np.asarray(Wqkv, dtype=np.float64).T
+    if bqkv is not None:
+        Y = Y + np.asarray(bqkv, dtype=np.float64)
+    Y = Y.reshape(B, L, 3, H, d)
+    return tuple(np.ascontiguousarray(Y[:, :, i].transpose(0, 2, 1, 3)) for i in range(3))
+
+
+def out_proj(O, Wo, bo):
+    """Y [B, L, C] = merge(O) W_o^T + b_o, merge: [B, H, L, d] -> [B, L, H * d]."""
+    O = np.asarray(O, dtype=np.float64)
+    B, H, L, d = O.shape
+    Om = O.transpose(0, 2, 1, 3).reshape(B, L, H * d)
+    Y = Om @ np.asarray(Wo, dtype=np.float64).T
+    if bo is not None:
+        Y = Y + np.asarray(bo, dtype=np.float64)
+    return Y
+
+
+class ModuleWeights:
+    """Weights of one attention module: W_qkv [3C, C], b_qkv [3C], W_o [C, C], b_o [C]."""
+
+    def __init__(self, Wqkv, bqkv, Wo, bo, H: int):
+        self.Wqkv, self.bqkv, self.Wo, self.bo, self.H = Wqkv, bqkv, Wo, bo, H
+
+
+class ModuleCache:
+    """Per-module state: the residual of the latest refresh (R, in the space of
+    the attention output before the output projection, as Eq. 1-2 define it)
+    and the module output of the latest non-AST step (Y_cache)."""
+
+    def __init__(self):
+        self.R = None
+        self.Y_cache = None
+
+
+def module_step(code: int, X, wts: ModuleWeights, cache: ModuleCache, w: int) -> np.ndarray:
+    """One attention module at one step under the plan (Sec. 3.2-3.5).
+
+    AST skips the whole module (its output is the cached module output,
+    Sec. 3.3).  ASC and WA-RS + ASC evaluate the module, projections
+    included, on the conditional half only and reuse its output for the
+    unconditional half (Sec. 3.4).  Every other code runs the projections
+    around the attention step of plan_step's table."""
+    if code == AST_REUSE:
+        if cache.Y_cache is None:
+            raise ValueError("AST before any cached output")
+        return np.array(cache.Y_cache, dtype=np.float64, copy=True)
+    X = np.asarray(X, dtype=np.float64)
+    B = X.shape[0]
+    half_codes = (ASC_REUSE, WARS_ASC_REFRESH, WARS_ASC_REUSE)
+    Xc = X[: _cond_half(B)] if code in half_codes else X
+    Q, K, V = qkv_proj(Xc, wts.Wqkv, wts.bqkv, wts.H)
+    if code in (FULL, ASC_REUSE):
+        O = attn_full(Q, K, V)
+    elif code in (WARS_REFRESH, WARS_ASC_REFRESH):
+        O, R = wars_refresh(Q, K, V, w)
+        cache.R = R
+    elif code in (WARS_REUSE, WARS_ASC_REUSE):
+        O = wars_reuse(Q, K, V, _residual_for(code, cache, B), w)
+    else:
+        raise ValueError(f"unknown plan code {code}")
+    Y = out_proj(O, wts.Wo, wts.bo)
+    if code in half_codes:
+        Y = np.concatenate([Y, Y], axis=0)
+    cache.Y_cache = Y
+    return Y
 
 
 # ---------------------------------------------------------------------------

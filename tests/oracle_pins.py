@@ -307,9 +307,99 @@ def pin_wars_asc():
     assert r_src[:, 0].tolist() == [-1, 0, -1, -1, 2] and o_src[:, 0].tolist() == [0, 1, 2, 2, 4]
 
 
+# P14 -- the attention module around the path: explicit loops for the two
+# projections; PyTorch's own multi-head attention module (fp64, CPU) for the
+# whole module with full and with band-masked attention; the module-level
+# sharing rules (ASC halves, AST cache, zero-drift WA-RS).
+def _module_weights(C, H, seed):
+    W = _rand((3 * C, C), seed, 1 / math.sqrt(C))
+    b = _rand((3 * C,), seed + 1, 0.5)
+    Wo = _rand((C, C), seed + 2, 1 / math.sqrt(C))
+    bo = _rand((C,), seed + 3, 0.5)
+    return O.ModuleWeights(W, b, Wo, bo, H)
+
+
+def _torch_mha(X, wts, band_w=None):
+    C = X.shape[2]
+    mha = torch.nn.MultiheadAttention(C, wts.H, batch_first=True, dtype=torch.float64)
+    with torch.no_grad():
+        mha.in_proj_weight.copy_(torch.from_numpy(wts.Wqkv))
+        mha.in_proj_bias.copy_(torch.from_numpy(wts.bqkv))
+        mha.out_proj.weight.copy_(torch.from_numpy(wts.Wo))
+        mha.out_proj.bias.copy_(torch.from_numpy(wts.bo))
+        t = torch.from_numpy(X)
+        mask = None
+        if band_w is not None:
+            i = torch.arange(X.shape[1])
+            mask = (i[:, None] - i[None, :]).abs() > band_w   # True = not attended
+        y, _ = mha(t, t, t, need_weights=False, attn_mask=mask)
+    return y.numpy()
+
+
+def pin_module():
+    # projections against explicit loops
+    B, L, H, d = 2, 5, 2, 4
+    C = H * d
+    wts = _module_weights(C, H, 160)
+    X = _rand((B, L, C), 164)
+    Q, K, V = O.qkv_proj(X, wts.Wqkv, wts.bqkv, H)
+    for b in range(B):
+        for l in range(L):
+            for f in range(3 * C):
+                acc = wts.bqkv[f]
+                for c in range(C):
+                    acc += X[b, l, c] * wts.Wqkv[f, c]
+                which, hd = divmod(f, C)
+                h, j = divmod(hd, d)
+                assert abs((Q, K, V)[which][b, h, l, j] - acc) <= 1e-12
+    Y = O.out_proj(Q, wts.Wo, wts.bo)
+    for b in range(B):
+        for l in range(L):
+            for n in range(C):
+                acc = wts.bo[n]
+                for h in range(H):
+                    for j in range(d):
+                        acc += Q[b, h, l, j] * wts.Wo[n, h * d + j]
+                assert abs(Y[b, l, n] - acc) <= 1e-12
+    # the whole module against torch's multi-head attention
+    B, L, H, d, w = 4, 19, 2, 8, 3
+    C = H * d
+    wts = _module_weights(C, H, 170)
+    X = _rand((B, L, C), 174)
+    Yf = O.module_step(O.FULL, X, wts, O.ModuleCache(), w)
+    assert np.max(np.abs(Yf - _torch_mha(X, wts))) <= 1e-12
+    cache = O.ModuleCache()
+    cache.R = np.zeros((B, H, L, d))
+    Yw = O.module_step(O.WARS_REUSE, X, wts, cache, w)
+    assert np.max(np.abs(Yw - _torch_mha(X, wts, band_w=w))) <= 1e-12
+    # sharing rules at module level
+    cache = O.ModuleCache()
+    Yr = O.module_step(O.WARS_REFRESH, X, wts, cache, w)
+    assert np.max(np.abs(Yr - Yf)) <= 1e-12 and cache.R.shape == (B, H, L, d)
+    assert np.max(np.abs(O.module_step(O.WARS_REUSE, X, wts, cache, w) - Yf)) <= 1e-12
+    Ya = O.module_step(O.ASC_REUSE, X, wts, cache, w)
+    assert np.array_equal(Ya[: B // 2], Ya[B // 2:])
+    assert np.max(np.abs(Ya[: B // 2] - Yf[: B // 2])) <= 1e-12
+    assert np.array_equal(O.module_step(O.AST_REUSE, None, wts, cache, w), Ya)
+    assert np.array_equal(cache.Y_cache, Ya)
+    Yh = O.module_step(O.WARS_ASC_REFRESH, X, wts, cache, w)
+    assert cache.R.shape[0] == B // 2 and np.array_equal(Yh[: B // 2], Yh[B // 2:])
+    assert np.max(np.abs(Yh[: B // 2] - Yf[: B // 2])) <= 1e-12
+    X2 = X + 0.05 * _rand(X.shape, 175)
+    Yu = O.module_step(O.WARS_ASC_REUSE, X2, wts, cache, w)
+    ref = O.module_step(O.WARS_REUSE, X2[: B // 2], wts, _with_r(cache.R), w)
+    assert np.max(np.abs(Yu[: B // 2] - ref)) <= 1e-12 and np.array_equal(Yu[: B // 2], Yu[B // 2:])
+
+
+def _with_r(R):
+    c = O.ModuleCache()
+    c.R = R
+    return c
+
+
 ALL_PINS = {
     "P1": pin_brute_force, "P2": pin_torch_sdpa, "P3": pin_wide_band, "P4": pin_zero_band,
     "P5": pin_zero_query, "P6": pin_constant_values, "P7": pin_probabilities,
     "P8": pin_refresh_reuse_algebra, "P9": pin_sharing, "P10": pin_permutation,
-    "P11": pin_table2, "P12": pin_plan, "P13": pin_wars_asc,
+    "P11": pin_table2, "P12": pin_plan, "P13": pin_wars_asc, "P14": pin_module,
 }

@@ -11,7 +11,7 @@ from oracle import dfa_oracle as O
 from tests import oracle_pins as pins
 
 # cheap pins first: a mutation stops at the first pin that catches it
-ORDER = ["P4", "P3", "P6", "P7", "P5", "P8", "P9", "P10", "P12", "P13", "P2", "P1", "P11"]
+ORDER = ["P4", "P3", "P6", "P7", "P5", "P8", "P9", "P10", "P12", "P13", "P14", "P2", "P1", "P11"]
 
 
 def _probs_factory(scale_fn=None, transpose=False, axis=-1):
@@ -94,6 +94,43 @@ def _residual_unchecked(code, cache, B):
     return cache.R if code == O.WARS_REUSE else cache.R[: B // 2]
 
 
+def _qkv_split_heads_first(X, Wqkv, bqkv, H):
+    X = np.asarray(X, dtype=np.float64)
+    B, L, C = X.shape
+    Y = (X @ np.asarray(Wqkv).T + bqkv).reshape(B, L, H, 3, C // H)   # (h, which) swapped
+    return tuple(np.ascontiguousarray(Y[:, :, :, i].transpose(0, 2, 1, 3)) for i in range(3))
+
+
+def _out_merge_dims_first(O_, Wo, bo):
+    O_ = np.asarray(O_, dtype=np.float64)
+    B, H, L, d = O_.shape
+    return O_.transpose(0, 2, 3, 1).reshape(B, L, H * d) @ np.asarray(Wo).T + bo   # (dim, head) order
+
+
+def _out_weight_transposed(O_, Wo, bo):
+    O_ = np.asarray(O_, dtype=np.float64)
+    B, H, L, d = O_.shape
+    return O_.transpose(0, 2, 1, 3).reshape(B, L, H * d) @ np.asarray(Wo) + bo
+
+
+def _qkv_no_bias(X, Wqkv, bqkv, H):
+    return _orig_qkv(X, Wqkv, None, H)
+
+
+_orig_qkv = O.qkv_proj
+_orig_module_step = O.module_step
+
+
+def _module_asc_projects_whole_batch(code, X, wts, cache, w):
+    if code == O.ASC_REUSE:
+        Y = O.out_proj(O.attn_full(*O.qkv_proj(X, wts.Wqkv, wts.bqkv, wts.H)), wts.Wo, wts.bo)
+        half = np.shape(X)[0] // 2
+        Y = np.concatenate([Y[half:], Y[half:]], axis=0)
+        cache.Y_cache = Y
+        return Y
+    return _orig_module_step(code, X, wts, cache, w)
+
+
 _orig_plan_step = O.plan_step
 
 
@@ -167,6 +204,11 @@ MUTATIONS = {
     "wars_asc_reuse_drops_residual": ("wars_asc_reuse", _wars_asc_reuse_no_residual),
     "wars_asc_reads_uncond_residual": ("_residual_for", _residual_wrong_half),
     "half_residual_feeds_full_reuse": ("_residual_for", _residual_unchecked),
+    "qkv_split_heads_first": ("qkv_proj", _qkv_split_heads_first),
+    "qkv_bias_dropped": ("qkv_proj", _qkv_no_bias),
+    "out_merge_dims_first": ("out_proj", _out_merge_dims_first),
+    "out_weight_transposed": ("out_proj", _out_weight_transposed),
+    "module_asc_uses_uncond_half": ("module_step", _module_asc_projects_whole_batch),
     "full_clears_residual": ("plan_step", _plan_step_full_clears_R),
     "splitmix_shift_typo": ("SplitMix64", _SplitMixTypo),
     "refresh_age_off_by_one": ("plan_make", _plan_age_off_by_one),
