@@ -135,6 +135,46 @@ dfa_status dfa_attn_window_plus_residual(const void* Q, const void* K, const voi
 dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, void* O, void* R,
                          void* Ocache, int B, int H, int L, int d, int w, hipStream_t stream);
 
+/* The attention module around the path (Sec. 3.1; the module whose FLOPs
+ * Table 2 counts): a fused QKV projection, attention, an output projection.
+ *   X, Y      [B][L][C] bf16 token-major hidden states, C = H * d
+ *   Wqkv      [3C][C] bf16, Linear layout (y = x W^T + b); output feature
+ *             f = which * C + head * d + dim with which 0/1/2 = q/k/v
+ *   bqkv      [3C] fp32 (may be NULL: no bias)
+ *   Wo, bo    [C][C] bf16 and [C] fp32 (bo may be NULL)
+ * Supported shapes: d in {64, 72} and C a multiple of 128 (else
+ * DFA_ERR_UNSUPPORTED).  Outputs must not overlap inputs or each other. */
+
+/* QKV projection: Q, K, V [B][H][L][d] = split(X Wqkv^T + bqkv). */
+dfa_status dfa_qkv_proj(const void* X, const void* Wqkv, const void* bqkv, void* Q, void* K, void* V,
+                        int B, int H, int L, int d, hipStream_t stream);
+
+/* Output projection: Y = merge(O) Wo^T + bo, merge reading O [B][H][L][d] as the
+ * [B][L][H * d] concatenation of heads. */
+dfa_status dfa_out_proj(const void* O, const void* Wo, const void* bo, void* Y, int B, int H, int L, int d,
+                        hipStream_t stream);
+
+/* One attention module of one layer at one step under plan `code` (the codes
+ * of dfa_plan_step), with the module-level caches:
+ *   AST          the whole module is skipped: Y = Ycache (a no-op when
+ *                Ycache == Y; X, weights and workspaces are not read and may
+ *                be NULL)
+ *   ASC, WARS_ASC_REFRESH, WARS_ASC_REUSE
+ *                the module, projections included, runs on the conditional
+ *                half (b < B/2) only; its output is stored to both halves
+ *                (Sec. 3.4).  B must be even.
+ *   other codes  QKV projection, the attention step of dfa_plan_step, output
+ *                projection, on the whole batch.
+ * Q, K, V, O are caller-owned [B][H][L][d] bf16 workspaces (the half-batch
+ * codes use their first halves); R is the layer's fp32 residual [B][H][L][d]
+ * in the space of the attention output before the output projection (Eq. 1-2;
+ * required by the four WA-RS codes, ignored otherwise).  Every computed step
+ * also writes its output to Ycache (unless Ycache is NULL or equal to Y).
+ * The kernels run back to back on `stream`. */
+dfa_status dfa_module_step(int code, const void* X, const void* Wqkv, const void* bqkv, const void* Wo,
+                           const void* bo, void* Q, void* K, void* V, void* O, void* R, void* Y, void* Ycache,
+                           int B, int H, int L, int d, int w, hipStream_t stream);
+
 /* Host only (no device is touched).  Draws a seeded per-(step, layer) plan in
  * place of the searched plan dictionary of Alg. 1 and resolves its cache
  * sources.  Output arrays are int32, step-major [n_steps][n_layers]:

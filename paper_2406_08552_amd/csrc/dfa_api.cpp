@@ -128,7 +128,7 @@ extern "C" {
 
 const char* dfa_last_error(void) { return g_last_error.c_str(); }
 
-const char* dfa_version(void) { return "0.1.0"; }
+const char* dfa_version(void) { return "0.2.0"; }
 
 dfa_status dfa_attn_full(const void* Q, const void* K, const void* V, void* O, void* R, int B, int H, int L, int d,
                          int w, hipStream_t stream) {
@@ -241,6 +241,204 @@ dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, 
             a.Rin = R;
             return hip_status(dfa::launch_window(a, stream), "WA-RS reuse launch");
     }
+}
+
+// ---------------------------------------------------------------------------
+// The attention module: projections and one module step
+// ---------------------------------------------------------------------------
+namespace {
+
+struct Region {
+    const void* p;
+    size_t n;
+    const char* name;
+};
+
+// every output region must avoid every input region and every other output
+dfa_status check_regions(const Region* outs, int nout, const Region* ins, int nin) {
+    for (int i = 0; i < nout; ++i) {
+        if (!outs[i].p) continue;
+        for (int j = 0; j < nin; ++j)
+            if (ins[j].p && overlaps(outs[i].p, outs[i].n, ins[j].p, ins[j].n))
+                return fail(DFA_ERR_INVALID_ARG, "%s overlaps %s", outs[i].name, ins[j].name);
+        for (int j = i + 1; j < nout; ++j)
+            if (outs[j].p && overlaps(outs[i].p, outs[i].n, outs[j].p, outs[j].n))
+                return fail(DFA_ERR_INVALID_ARG, "%s overlaps %s", outs[i].name, outs[j].name);
+    }
+    return DFA_OK;
+}
+
+dfa_status check_proj_shape(int B, int H, int L, int d, Shape* s) {
+    dfa_status st;
+    if ((st = check_shape(B, H, L, d, 0, s)) != DFA_OK) return st;
+    if (!dfa::proj_shape_supported(H, d))
+        return fail(DFA_ERR_UNSUPPORTED, "projection width H*d=%d is not a multiple of 128 (H=%d d=%d)", H * d, H, d);
+    return DFA_OK;
+}
+
+dfa_status check_bias(const void* b, const char* name) {
+    if (b && !aligned16(b)) return fail(DFA_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+    return DFA_OK;
+}
+
+}  // namespace
+
+dfa_status dfa_qkv_proj(const void* X, const void* Wqkv, const void* bqkv, void* Q, void* K, void* V, int B, int H,
+                        int L, int d, hipStream_t stream) {
+    Shape s;
+    dfa_status st;
+    if ((st = check_proj_shape(B, H, L, d, &s)) != DFA_OK) return st;
+    if ((st = check_ptr(X, "X")) != DFA_OK) return st;
+    if ((st = check_ptr(Wqkv, "Wqkv")) != DFA_OK) return st;
+    if ((st = check_bias(bqkv, "bqkv")) != DFA_OK) return st;
+    if ((st = check_qkv(Q, K, V)) != DFA_OK) return st;
+    const size_t C = (size_t)H * d;
+    const Region outs[] = {{Q, s.bytes, "Q"}, {K, s.bytes, "K"}, {V, s.bytes, "V"}};
+    const Region ins[] = {{X, s.bytes, "X"}, {Wqkv, 3 * C * C * 2, "Wqkv"}, {bqkv, 3 * C * 4, "bqkv"}};
+    if ((st = check_regions(outs, 3, ins, 3)) != DFA_OK) return st;
+    dfa::ProjLaunch a{};
+    a.W = Wqkv;
+    a.act = X;
+    a.bias = bqkv;
+    a.dst[0] = Q;
+    a.dst[1] = K;
+    a.dst[2] = V;
+    a.ndst = 3;
+    a.B = B;
+    a.H = H;
+    a.L = L;
+    a.d = d;
+    return hip_status(dfa::launch_qkv_proj(a, stream), "QKV projection launch");
+}
+
+dfa_status dfa_out_proj(const void* O, const void* Wo, const void* bo, void* Y, int B, int H, int L, int d,
+                        hipStream_t stream) {
+    Shape s;
+    dfa_status st;
+    if ((st = check_proj_shape(B, H, L, d, &s)) != DFA_OK) return st;
+    if ((st = check_ptr(O, "O")) != DFA_OK) return st;
+    if ((st = check_ptr(Wo, "Wo")) != DFA_OK) return st;
+    if ((st = check_bias(bo, "bo")) != DFA_OK) return st;
+    if ((st = check_ptr(Y, "Y")) != DFA_OK) return st;
+    const size_t C = (size_t)H * d;
+    const Region outs[] = {{Y, s.bytes, "Y"}};
+    const Region ins[] = {{O, s.bytes, "O"}, {Wo, C * C * 2, "Wo"}, {bo, C * 4, "bo"}};
+    if ((st = check_regions(outs, 1, ins, 3)) != DFA_OK) return st;
+    dfa::ProjLaunch a{};
+    a.W = Wo;
+    a.act = O;
+    a.bias = bo;
+    a.dst[0] = Y;
+    a.ndst = 1;
+    a.B = B;
+    a.H = H;
+    a.L = L;
+    a.d = d;
+    return hip_status(dfa::launch_out_proj(a, stream), "output projection launch");
+}
+
+dfa_status dfa_module_step(int code, const void* X, const void* Wqkv, const void* bqkv, const void* Wo, const void* bo,
+                           void* Q, void* K, void* V, void* O, void* R, void* Y, void* Ycache, int B, int H, int L,
+                           int d, int w, hipStream_t stream) {
+    if (code < DFA_FULL || code > DFA_WARS_ASC_REUSE) return fail(DFA_ERR_INVALID_ARG, "unknown plan code %d", code);
+    Shape s;
+    dfa_status st;
+    if ((st = check_proj_shape(B, H, L, d, &s)) != DFA_OK) return st;
+    if (w < 0) return fail(DFA_ERR_INVALID_ARG, "window half-width w=%d must be >= 0", w);
+    s.w = w;
+    if ((st = check_ptr(Y, "Y")) != DFA_OK) return st;
+    const bool sep = cache_is_separate(Y, Ycache);
+
+    if (code == DFA_AST_REUSE) {
+        // the whole module is skipped: only the cached module output is read
+        if (!Ycache) return fail(DFA_ERR_INVALID_ARG, "AST needs the module's output cache (Ycache is NULL)");
+        if (!sep) return DFA_OK;
+        if ((st = check_ptr(Ycache, "Ycache")) != DFA_OK) return st;
+        if (overlaps(Y, Ycache, s.bytes)) return fail(DFA_ERR_INVALID_ARG, "Ycache partially overlaps Y");
+        return hip_status(dfa::launch_copy(Ycache, Y, s.bytes, stream), "AST copy launch");
+    }
+
+    const bool half_batch = code == DFA_ASC_REUSE || code == DFA_WARS_ASC_REFRESH || code == DFA_WARS_ASC_REUSE;
+    if (half_batch && (B % 2)) return fail(DFA_ERR_INVALID_ARG, "plan code %d needs an even batch (B=%d)", code, B);
+    const bool uses_r = code == DFA_WARS_REFRESH || code == DFA_WARS_REUSE || code == DFA_WARS_ASC_REFRESH ||
+                        code == DFA_WARS_ASC_REUSE;
+    if ((st = check_ptr(X, "X")) != DFA_OK) return st;
+    if ((st = check_ptr(Wqkv, "Wqkv")) != DFA_OK) return st;
+    if ((st = check_ptr(Wo, "Wo")) != DFA_OK) return st;
+    if ((st = check_bias(bqkv, "bqkv")) != DFA_OK) return st;
+    if ((st = check_bias(bo, "bo")) != DFA_OK) return st;
+    if ((st = check_qkv(Q, K, V)) != DFA_OK) return st;
+    if ((st = check_ptr(O, "O")) != DFA_OK) return st;
+    if (uses_r && (st = check_ptr(R, "R")) != DFA_OK) return st;
+    if (sep && (st = check_ptr(Ycache, "Ycache")) != DFA_OK) return st;
+    const size_t C = (size_t)H * d;
+    const Region outs[] = {{Q, s.bytes, "Q"},
+                           {K, s.bytes, "K"},
+                           {V, s.bytes, "V"},
+                           {O, s.bytes, "O"},
+                           {uses_r ? R : nullptr, s.rbytes, "R"},
+                           {Y, s.bytes, "Y"},
+                           {sep ? Ycache : nullptr, s.bytes, "Ycache"}};
+    const Region ins[] = {{X, s.bytes, "X"},
+                          {Wqkv, 3 * C * C * 2, "Wqkv"},
+                          {bqkv, 3 * C * 4, "bqkv"},
+                          {Wo, C * C * 2, "Wo"},
+                          {bo, C * 4, "bo"}};
+    if ((st = check_regions(outs, 7, ins, 5)) != DFA_OK) return st;
+
+    const int Bc = half_batch ? B / 2 : B;
+    const size_t half = s.bytes / 2;
+    dfa::ProjLaunch pq{};
+    pq.W = Wqkv;
+    pq.act = X;
+    pq.bias = bqkv;
+    pq.dst[0] = Q;
+    pq.dst[1] = K;
+    pq.dst[2] = V;
+    pq.ndst = 3;
+    pq.B = Bc;
+    pq.H = H;
+    pq.L = L;
+    pq.d = d;
+    if ((st = hip_status(dfa::launch_qkv_proj(pq, stream), "QKV projection launch")) != DFA_OK) return st;
+
+    dfa::AttnLaunch a = make_launch(Q, K, V, s);
+    a.B = Bc;
+    a.dst[0] = O;
+    a.ndst = 1;
+    hipError_t e;
+    switch (code) {
+        case DFA_FULL:
+        case DFA_ASC_REUSE:
+            e = dfa::launch_full(a, stream);
+            break;
+        case DFA_WARS_REFRESH:
+        case DFA_WARS_ASC_REFRESH:
+            a.Rout = R;
+            e = dfa::launch_refresh(a, stream);
+            break;
+        default:  // DFA_WARS_REUSE, DFA_WARS_ASC_REUSE
+            a.Rin = R;
+            e = dfa::launch_window(a, stream);
+            break;
+    }
+    if ((st = hip_status(e, "module attention launch")) != DFA_OK) return st;
+
+    dfa::ProjLaunch po{};
+    po.W = Wo;
+    po.act = O;
+    po.bias = bo;
+    po.dst[po.ndst++] = Y;
+    if (half_batch) po.dst[po.ndst++] = (char*)Y + half;
+    if (sep) {
+        po.dst[po.ndst++] = Ycache;
+        if (half_batch) po.dst[po.ndst++] = (char*)Ycache + half;
+    }
+    po.B = Bc;
+    po.H = H;
+    po.L = L;
+    po.d = d;
+    return hip_status(dfa::launch_out_proj(po, stream), "output projection launch");
 }
 
 // ---------------------------------------------------------------------------

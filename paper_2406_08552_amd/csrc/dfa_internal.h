@@ -21,7 +21,22 @@ struct AttnLaunch {
     int B, H, L, d, w;
 };
 
+// One projection launch of the attention module over B * L tokens.
+//   QKV projection: act = X [B][L][H*d], W [3*H*d][H*d], dst[0..2] = Q, K, V
+//   output projection: act = O [B][H][L][d], W [H*d][H*d], dst[0..ndst) = copies of Y [B][L][H*d]
+struct ProjLaunch {
+    const void* W;
+    const void* act;
+    const void* bias;   // fp32, may be null
+    void* dst[4];
+    int ndst;
+    int B, H, L, d;
+};
+
 bool head_dim_supported(int d);
+bool proj_shape_supported(int H, int d);
+hipError_t launch_qkv_proj(const ProjLaunch& a, hipStream_t stream);
+hipError_t launch_out_proj(const ProjLaunch& a, hipStream_t stream);
 hipError_t launch_full(const AttnLaunch& a, hipStream_t stream);
 hipError_t launch_asc(const AttnLaunch& a, hipStream_t stream);  // full attention, separate kernel name
 hipError_t launch_refresh(const AttnLaunch& a, hipStream_t stream);

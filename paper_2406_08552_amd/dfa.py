@@ -29,7 +29,8 @@ CODE_NAMES = {FULL: "FULL", WARS_REFRESH: "WARS_REFRESH", WARS_REUSE: "WARS_REUS
 
 # every symbol include/dfa.h declares
 EXPORTS = ("dfa_attn_full", "dfa_attn_full_and_residual", "dfa_attn_window_plus_residual",
-           "dfa_plan_step", "dfa_plan_make", "dfa_last_error", "dfa_version")
+           "dfa_plan_step", "dfa_plan_make", "dfa_qkv_proj", "dfa_out_proj", "dfa_module_step",
+           "dfa_last_error", "dfa_version")
 
 
 class DfaError(RuntimeError):
@@ -59,6 +60,12 @@ def lib() -> ctypes.CDLL:
         L.dfa_plan_step.restype = _int
         L.dfa_plan_make.argtypes = [ctypes.c_uint64, _int, _int, _int, _int, _i32p, _i32p, _i32p]
         L.dfa_plan_make.restype = _int
+        L.dfa_qkv_proj.argtypes = [_vp] * 6 + [_int] * 4 + [_vp]
+        L.dfa_qkv_proj.restype = _int
+        L.dfa_out_proj.argtypes = [_vp] * 4 + [_int] * 4 + [_vp]
+        L.dfa_out_proj.restype = _int
+        L.dfa_module_step.argtypes = [_int] + [_vp] * 12 + [_int] * 5 + [_vp]
+        L.dfa_module_step.restype = _int
         L.dfa_last_error.argtypes = []
         L.dfa_last_error.restype = ctypes.c_char_p
         L.dfa_version.argtypes = []
@@ -130,6 +137,73 @@ def dfa_plan_step(code: int, Q, K, V, O, R, Ocache, w: int, stream=None) -> None
     B, H, L, d = _shape(O, Q, K, V, Ocache, R=R)
     _check(lib().dfa_plan_step(int(code), _ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(R), _ptr(Ocache),
                                B, H, L, d, w, _stream(stream)))
+
+
+def _expect(t, dtype, shape, name):
+    import torch
+    if t is None:
+        return
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or t.device.type != "cuda":
+        raise ValueError(f"{name}: expected a contiguous {dtype} GPU tensor of shape {tuple(shape)}, "
+                         f"got {t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+def _proj_shapes(X, Q):
+    """B, H, L, d from X [B, L, C] and a [B, H, L, d] tensor."""
+    B, H, L, d = Q.shape
+    if tuple(X.shape) != (B, L, H * d):
+        raise ValueError(f"X {tuple(X.shape)} does not match [B, L, H*d] = {(B, L, H * d)}")
+    return B, H, L, d
+
+
+def _weights(Wqkv, bqkv, Wo, bo, C):
+    import torch
+    _expect(Wqkv, torch.bfloat16, (3 * C, C), "Wqkv")
+    _expect(bqkv, torch.float32, (3 * C,), "bqkv")
+    _expect(Wo, torch.bfloat16, (C, C), "Wo")
+    _expect(bo, torch.float32, (C,), "bo")
+
+
+def dfa_qkv_proj(X, Wqkv, bqkv, Q, K, V, stream=None) -> None:
+    """Q, K, V = split(X Wqkv^T + bqkv); X [B, L, H*d] bf16, Q/K/V [B, H, L, d] bf16."""
+    import torch
+    B, H, L, d = _shape(Q, K, V)
+    _proj_shapes(X, Q)
+    _expect(X, torch.bfloat16, X.shape, "X")
+    _weights(Wqkv, bqkv, None, None, H * d)
+    _check(lib().dfa_qkv_proj(_ptr(X), _ptr(Wqkv), _ptr(bqkv), _ptr(Q), _ptr(K), _ptr(V), B, H, L, d, _stream(stream)))
+
+
+def dfa_out_proj(O, Wo, bo, Y, stream=None) -> None:
+    """Y = merge(O) Wo^T + bo; O [B, H, L, d] bf16, Y [B, L, H*d] bf16."""
+    import torch
+    B, H, L, d = _shape(O)
+    _proj_shapes(Y, O)
+    _expect(Y, torch.bfloat16, Y.shape, "Y")
+    _weights(None, None, Wo, bo, H * d)
+    _check(lib().dfa_out_proj(_ptr(O), _ptr(Wo), _ptr(bo), _ptr(Y), B, H, L, d, _stream(stream)))
+
+
+def dfa_module_step(code: int, X, Wqkv, bqkv, Wo, bo, Q, K, V, O, R, Y, Ycache, w: int, H: int,
+                    stream=None) -> None:
+    """One attention module with H heads under a plan code (see include/dfa.h).
+    Shapes come from Y [B, L, C] (d = C / H); for AST every other tensor may
+    be None."""
+    import torch
+    if Y is None or Y.dim() != 3:
+        raise ValueError("Y must be a [B, L, C] tensor")
+    B, L, C = Y.shape
+    if H <= 0 or C % H:
+        raise ValueError(f"C={C} is not a multiple of H={H}")
+    d = C // H
+    for t, name in ((X, "X"), (Y, "Y"), (Ycache, "Ycache")):
+        _expect(t, torch.bfloat16, (B, L, C), name)
+    for t, name in ((Q, "Q"), (K, "K"), (V, "V"), (O, "O")):
+        _expect(t, torch.bfloat16, (B, H, L, d), name)
+    _expect(R, torch.float32, (B, H, L, d), "R")
+    _weights(Wqkv, bqkv, Wo, bo, C)
+    _check(lib().dfa_module_step(int(code), _ptr(X), _ptr(Wqkv), _ptr(bqkv), _ptr(Wo), _ptr(bo), _ptr(Q), _ptr(K),
+                                 _ptr(V), _ptr(O), _ptr(R), _ptr(Y), _ptr(Ycache), B, H, L, d, w, _stream(stream)))
 
 
 def dfa_plan_make(seed: int, n_layers: int, n_steps: int, refresh_every: int, B: int):

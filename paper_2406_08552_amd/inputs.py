@@ -13,6 +13,12 @@ Recipe (stands in for the Q/K/V of a trained DiT; no dataset or weights):
   * each use rounds X_t to bf16 (round to nearest even).
 For bench-scale tensors ``device_qkv`` draws on the device with torch's
 seeded generator instead (same distribution, different stream).
+
+Attention-module inputs (random weights stand in for a trained DiT):
+  * hidden states X [B, L, C], C = H * d, follow the same drifting recipe
+    (tensor index 3);
+  * W_qkv [3C, C] and W_o [C, C] are N(0, 1/C) rounded to bf16, the biases
+    0.1 * N(0, 1) in fp32, from SeedSequence([240608552, 77, seed, k]).
 """
 from __future__ import annotations
 
@@ -95,6 +101,38 @@ class DriftingQKV:
             self.master = [m + np.float32(self.drift) * _normals(self.cfg_id, self.layer, t, i, self.shape)
                            for i, m in enumerate(self.master)]
         return to_bf16(self.master)
+
+
+class DriftingX:
+    """Hidden states [B, L, C] of one layer over steps 0, 1, 2, ... (fp32
+    masters, random walk with the given drift), rounded to bf16 per use."""
+
+    def __init__(self, cfg_id: int, layer: int, shape, drift: float = 0.05):
+        self.cfg_id, self.layer, self.shape, self.drift = cfg_id, layer, tuple(shape), drift
+        self.step = -1
+        self.master = None
+
+    def advance(self):
+        self.step += 1
+        z = _normals(self.cfg_id, self.layer, self.step, 3, self.shape)
+        self.master = z if self.step == 0 else self.master + np.float32(self.drift) * z
+        return to_bf16([self.master])[0]
+
+
+def module_weights(seed: int, H: int, d: int):
+    """(W_qkv bf16 [3C, C], b_qkv fp32 [3C], W_o bf16 [C, C], b_o fp32 [C]) CPU tensors."""
+    C = H * d
+
+    def normals(k, shape):
+        ss = np.random.SeedSequence([SEED_BASE, 77, seed, k])
+        return np.random.Generator(np.random.PCG64(ss)).standard_normal(shape, dtype=np.float32)
+
+    scale = np.float32(1.0 / np.sqrt(C))
+    Wqkv = to_bf16([normals(0, (3 * C, C)) * scale])[0]
+    Wo = to_bf16([normals(2, (C, C)) * scale])[0]
+    bqkv = torch.from_numpy(np.float32(0.1) * normals(1, (3 * C,)))
+    bo = torch.from_numpy(np.float32(0.1) * normals(3, (C,)))
+    return Wqkv, bqkv, Wo, bo
 
 
 def to_bf16(arrays):

@@ -135,3 +135,34 @@ def test_plan_odd_batch_and_bad_dims():
 
 def test_plan_null_arrays(L):
     assert L.dfa_plan_make(ctypes.c_uint64(1), 2, 2, 0, 2, None, None, None) == dfa.DFA_ERR_INVALID_ARG
+
+
+def test_projection_validation(L):
+    fq, fo, fm = L.dfa_qkv_proj, L.dfa_out_proj, L.dfa_module_step
+    big = 0x1000000
+    X, W, Q, K, V = (big * (i + 1) for i in range(5))
+    assert fq(X, W, None, Q, K, V, 2, 3, 64, 72, None) == dfa.DFA_ERR_UNSUPPORTED   # C = 216
+    assert "multiple of 128" in dfa.last_error()
+    assert fq(X, W, None, Q, K, V, 2, 16, 64, 80, None) == dfa.DFA_ERR_UNSUPPORTED
+    assert fq(None, W, None, Q, K, V, 2, 16, 64, 72, None) == dfa.DFA_ERR_INVALID_ARG
+    assert fq(X, W, X + 4, Q, K, V, 2, 16, 64, 72, None) == dfa.DFA_ERR_INVALID_ARG   # misaligned bias
+    assert fq(X, W, None, X, K, V, 2, 16, 64, 72, None) == dfa.DFA_ERR_INVALID_ARG    # Q aliases X
+    assert fq(X, W, None, Q, Q + 64, V, 2, 16, 64, 72, None) == dfa.DFA_ERR_INVALID_ARG  # K overlaps Q
+    assert fo(Q, W, None, Q, 2, 16, 64, 72, None) == dfa.DFA_ERR_INVALID_ARG           # Y aliases O
+    assert fo(Q, W, None, None, 2, 16, 64, 72, None) == dfa.DFA_ERR_INVALID_ARG
+    args = (2, 16, 64, 72, 8, None)
+    R, O, Y, Yc, Wo = (big * (i + 10) for i in range(5))
+    assert fm(9, X, W, None, Wo, None, Q, K, V, O, R, Y, Yc, *args) == dfa.DFA_ERR_INVALID_ARG   # code
+    assert fm(dfa.AST_REUSE, None, None, None, None, None, None, None, None, None, None, Y, None, *args) \
+        == dfa.DFA_ERR_INVALID_ARG
+    assert "Ycache" in dfa.last_error()
+    assert fm(dfa.AST_REUSE, None, None, None, None, None, None, None, None, None, None, Y, Y, *args) == dfa.DFA_OK
+    assert fm(dfa.ASC_REUSE, X, W, None, Wo, None, Q, K, V, O, R, Y, Yc, 3, 16, 64, 72, 8, None) \
+        == dfa.DFA_ERR_INVALID_ARG
+    assert "even" in dfa.last_error()
+    assert fm(dfa.WARS_REFRESH, X, W, None, Wo, None, Q, K, V, O, None, Y, Yc, *args) == dfa.DFA_ERR_INVALID_ARG
+    assert "R is NULL" in dfa.last_error()
+    assert fm(dfa.FULL, X, W, None, Wo, None, Q, K, V, Q, R, Y, Yc, *args) == dfa.DFA_ERR_INVALID_ARG  # O == Q
+    assert fm(dfa.FULL, X, W, None, Wo, None, Q, K, V, O, R, Y, Y + 64, *args) == dfa.DFA_ERR_INVALID_ARG
+    assert fm(dfa.FULL, X, W, None, Wo, None, Q, K, V, O, R, X, Yc, *args) == dfa.DFA_ERR_INVALID_ARG  # Y == X
+    assert fm(dfa.FULL, X, W, None, Wo, None, Q, K, V, O, R, Y, Yc, 2, 16, 64, 72, -1, None) == dfa.DFA_ERR_INVALID_ARG
