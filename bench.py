@@ -16,7 +16,10 @@ on their own next to the others.  Also reported:
 ms per layer-step of the plan run and of a full-attention-only run on the
 same inputs, per-kernel times, the roofline of the dominant kernel (the full
 attention kernel, measured with HIP events on its launch stream inside the
-timed region) and the fp64 CPU oracle timed on a bounded sample.
+timed region) and the fp64 CPU oracle timed on a bounded sample.  The
+`module` object reports the attention module around the path (QKV and
+output projections, module steps per plan code, the plan at module level),
+measured after the timed region.
 """
 from __future__ import annotations
 
@@ -67,6 +70,88 @@ def code_flops(code: int, B: int, H: int, L: int, d: int, w: int) -> float:
     full = 4.0 * B * H * L * L * d
     band = 4.0 * B * H * d * n_band(L, w)
     return {0: full, 1: full, 2: band, 3: 0.0, 4: full / 2, 5: full / 2, 6: band / 2}[code]
+
+
+def timed(torch, stream, fn, reps):
+    """Mean ms of fn() over reps calls, HIP events on the launch stream."""
+    fn()
+    torch.cuda.synchronize()
+    s0 = torch.cuda.Event(enable_timing=True)
+    s1 = torch.cuda.Event(enable_timing=True)
+    s0.record(stream)
+    for _ in range(reps):
+        fn()
+    s1.record(stream)
+    torch.cuda.synchronize()
+    return s0.elapsed_time(s1) / reps
+
+
+def module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres):
+    """The attention module around the path: projection GEMMs, one module step
+    per plan code, and the seeded plan executed at module level (28 layers,
+    per-layer hidden states, residuals and output caches; one weight set, as
+    the kernels' work does not depend on weight values)."""
+    B, H, L, d, w = cfg.B, cfg.H, cfg.L, cfg.d, cfg.w
+    C = H * d
+    NL, NS = cfg.n_layers, cfg.n_steps
+    Wqkv, bqkv, Wo, bo = (t.to(dev) for t in inputs.module_weights(cfg.cfg_id, H, d))
+    shape = (B, H, L, d)
+    Q, K, V, O = (torch.empty(shape, dtype=torch.bfloat16, device=dev) for _ in range(4))
+    X = [inputs.device_qkv(inputs.SEED_BASE + 5000 + l, (B, L, C), dev, n=1)[0] for l in range(NL)]
+    Y = [torch.empty((B, L, C), dtype=torch.bfloat16, device=dev) for _ in range(NL)]
+    R = [torch.empty(shape, dtype=torch.float32, device=dev) for _ in range(NL)]
+    torch.cuda.synchronize()
+    M = B * L
+    qkv_flops, out_flops = 2.0 * M * C * 3 * C, 2.0 * M * C * C
+    reps = args.kernel_reps
+    ms_qkv = timed(torch, stream, lambda: dfa.dfa_qkv_proj(X[0], Wqkv, bqkv, Q, K, V, stream), reps)
+    ms_out = timed(torch, stream, lambda: dfa.dfa_out_proj(O, Wo, bo, Y[0], stream), reps)
+
+    def step(c, l):
+        dfa.dfa_module_step(c, X[l], Wqkv, bqkv, Wo, bo, Q, K, V, O, R[l], Y[l], Y[l], w, H, stream)
+
+    step(dfa.WARS_REFRESH, 0)
+    per = {}
+    for c in (dfa.FULL, dfa.WARS_REFRESH, dfa.WARS_REUSE, dfa.ASC_REUSE, dfa.WARS_ASC_REUSE, dfa.AST_REUSE):
+        per[dfa.CODE_NAMES[c].lower()] = round(timed(torch, stream, lambda c=c: step(c, 0), reps), 4)
+
+    def module_pass(codes):
+        for t in range(NS):
+            for l in range(NL):
+                step(int(codes[t, l]), l)
+
+    module_pass(code)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    e0.record(stream)
+    module_pass(code)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    plan_ms = max(e0.elapsed_time(e1), (time.perf_counter() - w0) * 1e3)
+    full_codes = code.copy()
+    full_codes[:] = dfa.FULL
+    w0 = time.perf_counter()
+    e0.record(stream)
+    module_pass(full_codes)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    full_ms = max(e0.elapsed_time(e1), (time.perf_counter() - w0) * 1e3)
+    return {
+        "shape": {"tokens": M, "C": C, "qkv_weight": [3 * C, C], "out_weight": [C, C]},
+        "qkv_proj": {"ms": round(ms_qkv, 4), "tflops": round(qkv_flops / (ms_qkv * 1e-3) / 1e12, 1)},
+        "out_proj": {"ms": round(ms_out, 4), "tflops": round(out_flops / (ms_out * 1e-3) / 1e12, 1)},
+        "ms_per_module_step": per,
+        # module time of each strategy's compressed step relative to the
+        # uncompressed module (Table 2's latency rows are module-level)
+        "latency_fraction_vs_full": {
+            name: round(per[key] / per["full"], 4)
+            for name, key in (("asc", "asc_reuse"), ("wars", "wars_reuse"), ("wars_asc", "wars_asc_reuse"),
+                              ("ast", "ast_reuse"))},
+        "plan_ms_per_layer_step": round(plan_ms / (NL * NS), 4),
+        "full_only_ms_per_layer_step": round(full_ms / (NL * NS), 4),
+        "plan_speedup_vs_full_only": round(full_ms / plan_ms, 3),
+    }
 
 
 def parse():
@@ -231,6 +316,8 @@ def main():
         kres[name] = {"ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 1) if fl else 0.0,
                       "gbs": round(ntens * tensor_bytes / (ms * 1e-3) / 1e9, 1)}
 
+    module = module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres)
+
     full_ms = sum(per_code.get(0, [])) / max(1, len(per_code.get(0, [])))
     full_flops = code_flops(0, B, H, L, d, w)
     achieved = full_flops / (full_ms * 1e-3) / 1e12 if full_ms > 0 else 0.0
@@ -266,6 +353,7 @@ def main():
                               ("ast", "ast_copy"))},
         "full_equiv_tflops": round(plan_layer_steps * full_flops / (ms_per_step * 1e-3) / 1e12, 1),
         "kernels": kres,
+        "module": module,
         "reuse_speedup_vs_full": round(kres["full"]["ms"] / kres["wars_reuse"]["ms"], 3),
         "reuse_ideal_speedup": round(L * L / n_band(L, w), 3),
         "roofline": {"kernel": "attn_kernel<72, FULL> (dfa_attn_full / FULL plan entries)", "bound": "mfma",
