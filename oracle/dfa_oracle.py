@@ -523,6 +523,99 @@ def module_step(code: int, X, wts: ModuleWeights, cache: ModuleCache, w: int, st
 
 
 # ---------------------------------------------------------------------------
+# Plan search (Sec. 3.5, Alg. 1) on a surrogate model
+# ---------------------------------------------------------------------------
+MRAE_EPS = 1e-6
+
+
+def mrae(O, O2, eps: float = MRAE_EPS) -> float:
+    """Mean relative absolute error of Sec. 3.5 / appendix: the mean over all
+    elements of clip(|O_i - O'_i| / (max(|O_i|, |O'_i|) + eps), 0, 10)."""
+    a = np.asarray(O, dtype=np.float64).ravel()
+    b = np.asarray(O2, dtype=np.float64).ravel()
+    r = np.abs(a - b) / (np.maximum(np.abs(a), np.abs(b)) + eps)
+    return float(np.mean(np.clip(r, 0.0, 10.0)))
+
+
+# The compression strategies of Alg. 1's list S, as module-level plan codes.
+SEARCH_STRATEGIES = (AST_REUSE, WARS_ASC_REUSE, WARS_REUSE, ASC_REUSE)
+
+
+def strategy_order(L: int, C: int, w: int):
+    """S ordered from the largest computation reduction to the smallest (Alg. 1
+    iterates the list in this order and keeps the first strategy that meets
+    the threshold, i.e. the one with the highest reduction): AST computes
+    nothing, ASC half the module, WA-RS the projections plus the band,
+    WA-RS + ASC half of that.  Ties keep the order of the list above."""
+    wars = module_attn_flops_fraction(L, C, w, share_cfg=False)
+    frac = {AST_REUSE: 0.0, WARS_ASC_REUSE: wars / 2, WARS_REUSE: wars, ASC_REUSE: 0.5}
+    return tuple(sorted(SEARCH_STRATEGIES, key=lambda c: (frac[c], SEARCH_STRATEGIES.index(c))))
+
+
+def surrogate_forward(X, layers, codes, caches, w: int, first: int = 0, store=None):
+    """The surrogate DiT: hidden states pass through the attention modules
+    layers[first:], each with a residual connection, X <- X + module(X);
+    codes[i] is layer i's plan code and caches[i] its module cache.  Returns
+    the model output."""
+    X = np.asarray(X, dtype=np.float64)
+    for i in range(first, len(layers)):
+        X = X + module_step(codes[i], X, layers[i], caches[i], w, store=store)
+    return X
+
+
+def _applicable(code: int, cache: ModuleCache, B: int) -> bool:
+    if code == AST_REUSE:
+        return cache.Y_cache is not None
+    if code in (WARS_REUSE, WARS_ASC_REUSE):
+        # the residual of a whole-batch refresh (the search refreshes whole batches)
+        return cache.R is not None and np.shape(cache.R)[0] == B and (code == WARS_REUSE or B % 2 == 0)
+    return B % 2 == 0   # ASC
+
+
+def plan_search(X_steps, layers, delta: float, w: int, store=None):
+    """Alg. 1: for each step t, the output O of the uncompressed model; then
+    for each layer i (1-based index in the threshold) the strategies of S in
+    order, each applied to layer i alone on top of the strategies already
+    chosen for layers < i at this step (layers > i uncompressed); the first
+    with L(O, O') < (i / |M|) delta is kept, else the layer is not compressed.
+    An uncompressed layer runs as a WA-RS refresh, so that it is the residual
+    source of later reuse steps; trial runs leave the caches untouched and a
+    layer's cache is updated once its strategy is chosen.
+
+    Returns (plan [T, |M|] int32, loss [T, |M|]: the accepted strategy's loss,
+    or nan where the layer was not compressed)."""
+    n_layers = len(layers)
+    X0 = np.asarray(X_steps[0], dtype=np.float64)
+    B, L, C = X0.shape
+    order = strategy_order(L, C, w)
+    caches = [ModuleCache() for _ in range(n_layers)]
+    T = len(X_steps)
+    plan = np.full((T, n_layers), -1, dtype=np.int32)
+    loss = np.full((T, n_layers), np.nan)
+    import copy
+    for t in range(T):
+        X = np.asarray(X_steps[t], dtype=np.float64)
+        scratch = [ModuleCache() for _ in range(n_layers)]
+        O_ref = surrogate_forward(X, layers, [FULL] * n_layers, scratch, w, store=store)
+        for i in range(n_layers):
+            chosen = WARS_REFRESH
+            for m in order:
+                if not _applicable(m, caches[i], B):
+                    continue
+                trial = copy.deepcopy(caches[i])
+                Xi = X + module_step(m, X, layers[i], trial, w, store=store)
+                rest = [ModuleCache() for _ in range(n_layers)]
+                O2 = surrogate_forward(Xi, layers, [FULL] * n_layers, rest, w, first=i + 1, store=store)
+                lv = mrae(O_ref, O2)
+                if lv < (i + 1) / n_layers * delta:
+                    chosen, loss[t, i] = m, lv
+                    break
+            plan[t, i] = chosen
+            X = X + module_step(chosen, X, layers[i], caches[i], w, store=store)
+    return plan, loss
+
+
+# ---------------------------------------------------------------------------
 # Attention-FLOP accounting (Table 2)
 # ---------------------------------------------------------------------------
 def core_attention_flops(B: int, H: int, L: int, d: int, pairs: int | None = None) -> int:

@@ -397,9 +397,100 @@ def _with_r(R):
     return c
 
 
+# P15 -- MRAE loss and the greedy plan search (Sec. 3.5, Alg. 1): the loss on a
+# hand-worked example, by explicit loops and in closed-form cases; the search
+# in its degenerate cases (delta = 0, unbounded delta, zero drift, identical
+# CFG halves); and every decision of a searched plan re-evaluated through
+# plain full-model forwards with replayed caches.
+def _surrogate(B, L, H, d, n_layers, seed, drift=0.02, T=4, cfg_same=False):
+    C = H * d
+    layers = []
+    for i in range(n_layers):
+        wts = _module_weights(C, H, seed + 10 * i)
+        wts.Wo = wts.Wo * 0.5
+        layers.append(wts)
+    X = _rand((B, L, C), seed + 500)
+    if cfg_same:
+        X[B // 2:] = X[: B // 2]
+    Xs = [X]
+    for t in range(1, T):
+        Z = _rand((B, L, C), seed + 500 + t)
+        if cfg_same:
+            Z[B // 2:] = Z[: B // 2]
+        Xs.append(Xs[-1] + drift * Z)
+    return Xs, layers
+
+
+def _replay_check(Xs, layers, plan, delta, w):
+    """Replays the plan step by step; at each (t, i) the chosen strategy's
+    loss, evaluated through a plain forward of the whole model, is below the
+    threshold and every strategy earlier in the order that applied is not."""
+    import copy
+    n = len(layers)
+    B, L, C = np.shape(Xs[0])
+    order = O.strategy_order(L, C, w)
+    caches = [O.ModuleCache() for _ in range(n)]
+    for t, X in enumerate(Xs):
+        O_ref = O.surrogate_forward(X, layers, [O.FULL] * n, [O.ModuleCache() for _ in range(n)], w)
+        for i in range(n):
+            chosen = int(plan[t, i])
+            thr = (i + 1) / n * delta
+            for m in order:
+                if not O._applicable(m, caches[i], B):
+                    assert m != chosen
+                    continue
+                trial = [copy.deepcopy(c) for c in caches]
+                codes = [int(c) for c in plan[t, :i]] + [m] + [O.FULL] * (n - i - 1)
+                lv = O.mrae(O_ref, O.surrogate_forward(X, layers, codes, trial, w))
+                if m == chosen:
+                    assert lv < thr, (t, i, m, lv, thr)
+                    break
+                assert lv >= thr, (t, i, m, lv, thr)
+            else:
+                assert chosen == O.WARS_REFRESH, (t, i, chosen)
+        O.surrogate_forward(X, layers, [int(c) for c in plan[t]], caches, w)
+
+
+def pin_search():
+    # MRAE
+    a = np.array([1.0, 2.0, -1.0, 0.0, 3.0])
+    b = np.array([1.5, 2.0, 1.0, 0.0, -0.5])
+    hand = (0.5 / 1.5 + 0 + 2 / 1 + 0 + 3.5 / 3) / 5   # the (0, 0) pair counts 0 / eps = 0
+    assert abs(O.mrae(a, b) - hand) <= 1e-6
+    x, y = _rand((3, 7), 181), _rand((3, 7), 182)
+    tot = 0.0
+    for i in range(3):
+        for j in range(7):
+            tot += min(10.0, max(0.0, abs(x[i, j] - y[i, j]) / (max(abs(x[i, j]), abs(y[i, j])) + 1e-6)))
+    assert abs(O.mrae(x, y) - tot / 21) <= 1e-14
+    assert O.mrae(x, x) == 0.0
+    assert abs(O.mrae(x, -x) - 2.0) <= 1e-5 and abs(O.mrae(x, np.zeros_like(x)) - 1.0) <= 1e-5
+    assert O.mrae(np.zeros(4), np.zeros(4)) == 0.0
+    # strategy order: the list of Sec. 3.5 at 16K tokens; ASC before WA-RS at 1K (Table 2)
+    assert O.strategy_order(16384, 1152, 2048) == (O.AST_REUSE, O.WARS_ASC_REUSE, O.WARS_REUSE, O.ASC_REUSE)
+    assert O.strategy_order(1024, 1152, 128) == (O.AST_REUSE, O.WARS_ASC_REUSE, O.ASC_REUSE, O.WARS_REUSE)
+    # degenerate cases of the search
+    B, L, H, d, w, n = 2, 24, 2, 8, 3, 3
+    Xs, layers = _surrogate(B, L, H, d, n, 190)
+    plan, loss = O.plan_search(Xs, layers, 0.0, w)
+    assert np.all(plan == O.WARS_REFRESH) and np.all(np.isnan(loss))
+    plan, _ = O.plan_search(Xs, layers, 1e30, w)
+    assert np.all(plan[0] == O.ASC_REUSE) and np.all(plan[1:] == O.AST_REUSE)
+    plan, loss = O.plan_search([Xs[0]] * 3, layers, 1e-12, w)
+    assert np.all(plan[0] == O.WARS_REFRESH) and np.all(plan[1:] == O.AST_REUSE) and np.all(loss[1:] == 0.0)
+    Xc, _ = _surrogate(B, L, H, d, n, 190, cfg_same=True)
+    plan, loss = O.plan_search(Xc[:1], layers, 1e-12, w)
+    assert np.all(plan[0] == O.ASC_REUSE) and np.all(loss[0] == 0.0)
+    # every decision of a searched plan, replayed through whole-model forwards
+    for delta in (0.05, 0.2):
+        plan, _ = O.plan_search(Xs, layers, delta, w)
+        _replay_check(Xs, layers, plan, delta, w)
+
+
 ALL_PINS = {
     "P1": pin_brute_force, "P2": pin_torch_sdpa, "P3": pin_wide_band, "P4": pin_zero_band,
     "P5": pin_zero_query, "P6": pin_constant_values, "P7": pin_probabilities,
     "P8": pin_refresh_reuse_algebra, "P9": pin_sharing, "P10": pin_permutation,
     "P11": pin_table2, "P12": pin_plan, "P13": pin_wars_asc, "P14": pin_module,
+    "P15": pin_search,
 }

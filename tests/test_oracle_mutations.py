@@ -11,7 +11,7 @@ from oracle import dfa_oracle as O
 from tests import oracle_pins as pins
 
 # cheap pins first: a mutation stops at the first pin that catches it
-ORDER = ["P4", "P3", "P6", "P7", "P5", "P8", "P9", "P10", "P12", "P13", "P14", "P2", "P1", "P11"]
+ORDER = ["P4", "P3", "P6", "P7", "P5", "P8", "P9", "P10", "P12", "P13", "P14", "P15", "P2", "P1", "P11"]
 
 
 def _probs_factory(scale_fn=None, transpose=False, axis=-1):
@@ -131,6 +131,97 @@ def _module_asc_projects_whole_batch(code, X, wts, cache, w):
     return _orig_module_step(code, X, wts, cache, w)
 
 
+def _mrae_no_abs(Oa, Ob, eps=O.MRAE_EPS):
+    a = np.asarray(Oa, dtype=np.float64).ravel()
+    b = np.asarray(Ob, dtype=np.float64).ravel()
+    return float(np.mean(np.clip((a - b) / (np.maximum(a, b) + eps), 0.0, 10.0)))
+
+
+def _mrae_min_norm(Oa, Ob, eps=O.MRAE_EPS):
+    a = np.asarray(Oa, dtype=np.float64).ravel()
+    b = np.asarray(Ob, dtype=np.float64).ravel()
+    return float(np.mean(np.clip(np.abs(a - b) / (np.minimum(np.abs(a), np.abs(b)) + eps), 0.0, 10.0)))
+
+
+def _order_reversed(L, C, w):
+    return tuple(reversed(_orig_order(L, C, w)))
+
+
+_orig_order = O.strategy_order
+_orig_search = O.plan_search
+
+
+def _search_zero_based_threshold(X_steps, layers, delta, w, store=None):
+    # (i / |M|) delta with a 0-based layer index: layer 0 can never be compressed
+    import copy
+    n_layers = len(layers)
+    B, L, C = np.shape(X_steps[0])
+    order = O.strategy_order(L, C, w)
+    caches = [O.ModuleCache() for _ in range(n_layers)]
+    plan = np.full((len(X_steps), n_layers), -1, dtype=np.int32)
+    loss = np.full(plan.shape, np.nan)
+    for t, X in enumerate(X_steps):
+        X = np.asarray(X, dtype=np.float64)
+        O_ref = O.surrogate_forward(X, layers, [O.FULL] * n_layers, [O.ModuleCache() for _ in layers], w)
+        for i in range(n_layers):
+            chosen = O.WARS_REFRESH
+            for m in order:
+                if not O._applicable(m, caches[i], B):
+                    continue
+                trial = copy.deepcopy(caches[i])
+                Xi = X + O.module_step(m, X, layers[i], trial, w)
+                O2 = O.surrogate_forward(Xi, layers, [O.FULL] * n_layers, [O.ModuleCache() for _ in layers], w,
+                                         first=i + 1)
+                if O.mrae(O_ref, O2) < i / n_layers * delta:
+                    chosen = m
+                    break
+            plan[t, i] = chosen
+            X = X + O.module_step(chosen, X, layers[i], caches[i], w)
+    return plan, loss
+
+
+def _search_stale_reference(X_steps, layers, delta, w, store=None):
+    # the uncompressed output of step 0 serves as the reference of every step
+    return _search_with_reference(X_steps, layers, delta, w, stale=True)
+
+
+def _search_commit_full(X_steps, layers, delta, w, store=None):
+    # uncompressed layers committed as FULL: no residual is ever refreshed
+    return _search_with_reference(X_steps, layers, delta, w, commit_full=True)
+
+
+def _search_with_reference(X_steps, layers, delta, w, stale=False, commit_full=False):
+    import copy
+    n_layers = len(layers)
+    B, L, C = np.shape(X_steps[0])
+    order = O.strategy_order(L, C, w)
+    caches = [O.ModuleCache() for _ in range(n_layers)]
+    plan = np.full((len(X_steps), n_layers), -1, dtype=np.int32)
+    loss = np.full(plan.shape, np.nan)
+    O_first = None
+    for t, X in enumerate(X_steps):
+        X = np.asarray(X, dtype=np.float64)
+        O_ref = O.surrogate_forward(X, layers, [O.FULL] * n_layers, [O.ModuleCache() for _ in layers], w)
+        if stale:
+            O_first = O_ref if O_first is None else O_first
+            O_ref = O_first
+        for i in range(n_layers):
+            chosen = O.FULL if commit_full else O.WARS_REFRESH
+            for m in order:
+                if not O._applicable(m, caches[i], B):
+                    continue
+                trial = copy.deepcopy(caches[i])
+                Xi = X + O.module_step(m, X, layers[i], trial, w)
+                O2 = O.surrogate_forward(Xi, layers, [O.FULL] * n_layers, [O.ModuleCache() for _ in layers], w,
+                                         first=i + 1)
+                if O.mrae(O_ref, O2) < (i + 1) / n_layers * delta:
+                    chosen = m
+                    break
+            plan[t, i] = chosen
+            X = X + O.module_step(chosen, X, layers[i], caches[i], w)
+    return plan, loss
+
+
 _orig_plan_step = O.plan_step
 
 
@@ -209,6 +300,12 @@ MUTATIONS = {
     "out_merge_dims_first": ("out_proj", _out_merge_dims_first),
     "out_weight_transposed": ("out_proj", _out_weight_transposed),
     "module_asc_uses_uncond_half": ("module_step", _module_asc_projects_whole_batch),
+    "mrae_without_abs": ("mrae", _mrae_no_abs),
+    "mrae_min_normaliser": ("mrae", _mrae_min_norm),
+    "search_order_reversed": ("strategy_order", _order_reversed),
+    "search_zero_based_threshold": ("plan_search", _search_zero_based_threshold),
+    "search_stale_reference": ("plan_search", _search_stale_reference),
+    "search_commit_full": ("plan_search", _search_commit_full),
     "full_clears_residual": ("plan_step", _plan_step_full_clears_R),
     "splitmix_shift_typo": ("SplitMix64", _SplitMixTypo),
     "refresh_age_off_by_one": ("plan_make", _plan_age_off_by_one),
