@@ -86,6 +86,28 @@ def timed(torch, stream, fn, reps):
     return s0.elapsed_time(s1) / reps
 
 
+def search_bench(args, dfa, inputs, torch, dev, stream):
+    """The greedy plan search (Alg. 1) on a 28-layer surrogate of DiT-XL/2 at
+    512 px (B = 8 as four CFG pairs, L = 1024, H = 16, d = 72, band half-width
+    128, random weights), over a few denoising steps."""
+    cfg = inputs.CONFIGS["dit512"]
+    B, H, L, d, w, NL = cfg.B, cfg.H, cfg.L, cfg.d, cfg.w, cfg.n_layers
+    T = args.search_steps
+    if T <= 0:
+        return None
+    Xs = [x.to(dev) for x in inputs.surrogate_states(cfg.cfg_id, B, L, H * d, T, 0.05)]
+    layers = [tuple(t.to(dev) for t in inputs.module_weights(200 + i, H, d)) for i in range(NL)]
+    ws = torch.empty(dfa.plan_search_workspace_bytes(NL, B, H, L, d), dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    plan, loss = dfa.dfa_plan_search(Xs, layers, args.search_delta, w, H, ws, stream)
+    sec = time.perf_counter() - t0
+    del ws
+    return {"workload": "dit_xl2_512px surrogate", "layers": NL, "steps": T, "delta": args.search_delta,
+            "seconds": round(sec, 3), "seconds_per_step": round(sec / T, 3),
+            "plan_code_counts": {dfa.CODE_NAMES[c].lower(): int((plan == c).sum()) for c in sorted(set(plan.flat))}}
+
+
 def module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres):
     """The attention module around the path: projection GEMMs, one module step
     per plan code, and the seeded plan executed at module level (28 layers,
@@ -137,7 +159,9 @@ def module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres):
     e1.record(stream)
     torch.cuda.synchronize()
     full_ms = max(e0.elapsed_time(e1), (time.perf_counter() - w0) * 1e3)
+    search = search_bench(args, dfa, inputs, torch, dev, stream)
     return {
+        "search": search,
         "shape": {"tokens": M, "C": C, "qkv_weight": [3 * C, C], "out_weight": [C, C]},
         "qkv_proj": {"ms": round(ms_qkv, 4), "tflops": round(qkv_flops / (ms_qkv * 1e-3) / 1e12, 1)},
         "out_proj": {"ms": round(ms_out, 4), "tflops": round(out_flops / (ms_out * 1e-3) / 1e12, 1)},
@@ -163,6 +187,8 @@ def parse():
     ap.add_argument("--kernel-reps", type=int, default=10)
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--search-steps", type=int, default=3, help="denoising steps of the plan-search measurement")
+    ap.add_argument("--search-delta", type=float, default=0.1)
     return ap.parse_args()
 
 

@@ -48,6 +48,7 @@
 #ifndef DFA_H
 #define DFA_H
 
+#include <stddef.h>
 #include <stdint.h>
 #include <hip/hip_runtime_api.h>
 
@@ -174,6 +175,46 @@ dfa_status dfa_out_proj(const void* O, const void* Wo, const void* bo, void* Y, 
 dfa_status dfa_module_step(int code, const void* X, const void* Wqkv, const void* bqkv, const void* Wo,
                            const void* bo, void* Q, void* K, void* V, void* O, void* R, void* Y, void* Ycache,
                            int B, int H, int L, int d, int w, hipStream_t stream);
+
+/* Mean relative absolute error of the plan search (Sec. 3.5):
+ *   L(A, B) = mean_i clip(|A_i - B_i| / (max(|A_i|, |B_i|) + 1e-6), 0, 10)
+ * over n bf16 elements (DEVICE pointers, 16-byte aligned).  The result is
+ * written as one fp64 value to the DEVICE pointer `result` (8-byte aligned).  `workspace` is a
+ * caller-owned DEVICE buffer of DFA_MRAE_WORKSPACE_BYTES (per-workgroup
+ * partial sums; calls that share it must not overlap).  Each lane sums its
+ * share in fp32, the partial sums are added in fp64 in a fixed order: the
+ * result is deterministic. */
+#define DFA_MRAE_WORKSPACE_BYTES 8192
+dfa_status dfa_mrae(const void* A, const void* B, size_t n, void* workspace, double* result, hipStream_t stream);
+
+/* Bytes of DEVICE workspace dfa_plan_search needs (0 for bad sizes). */
+size_t dfa_plan_search_workspace_bytes(int n_layers, int B, int H, int L, int d);
+
+/* The greedy plan search of Alg. 1 (Sec. 3.5) on a surrogate model: a stack of
+ * n_layers attention modules (dfa_module_step), each with a residual
+ * connection, X <- X + module_i(X), evaluated at the hidden states
+ * X_steps[t] ([B][L][C] bf16 DEVICE pointers, one per denoising step).
+ * Per step t the output O of the uncompressed model is formed; then for each
+ * layer i the strategies AST, WA-RS + ASC, WA-RS, ASC, ordered from the
+ * largest computation reduction to the smallest (the module FLOP fractions at
+ * this L, C and w; ties keep that order), are applied to layer i alone on top
+ * of the choices already made for layers < i at this step, and the first with
+ * dfa_mrae(O, O') < ((i + 1) / n_layers) * delta is kept.  An uncompressed
+ * layer runs as DFA_WARS_REFRESH, so it is the residual source of later reuse
+ * steps; WA-RS needs such a refresh, AST a computed step before, ASC an even B.
+ *   Wqkv, bqkv, Wo, bo  HOST arrays of n_layers DEVICE pointers (bqkv, bo may
+ *                       be NULL arrays: no biases)
+ *   workspace           caller-owned DEVICE buffer, 256-byte aligned, of at
+ *                       least dfa_plan_search_workspace_bytes() (module caches
+ *                       and scratch; its contents are overwritten)
+ *   plan, loss          HOST outputs [n_steps][n_layers]: the plan code per
+ *                       layer and step, and the accepted strategy's loss (NaN
+ *                       where the layer is not compressed)
+ * The host loop synchronises `stream` after each loss evaluation. */
+dfa_status dfa_plan_search(int n_layers, int n_steps, const void* const* X_steps, const void* const* Wqkv,
+                           const void* const* bqkv, const void* const* Wo, const void* const* bo, double delta,
+                           int B, int H, int L, int d, int w, void* workspace, size_t workspace_bytes,
+                           int32_t* plan, double* loss, hipStream_t stream);
 
 /* Host only (no device is touched).  Draws a seeded per-(step, layer) plan in
  * place of the searched plan dictionary of Alg. 1 and resolves its cache

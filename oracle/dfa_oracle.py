@@ -557,9 +557,10 @@ def surrogate_forward(X, layers, codes, caches, w: int, first: int = 0, store=No
     layers[first:], each with a residual connection, X <- X + module(X);
     codes[i] is layer i's plan code and caches[i] its module cache.  Returns
     the model output."""
+    keep = store if store is not None else (lambda a: a)
     X = np.asarray(X, dtype=np.float64)
     for i in range(first, len(layers)):
-        X = X + module_step(codes[i], X, layers[i], caches[i], w, store=store)
+        X = keep(X + module_step(codes[i], X, layers[i], caches[i], w, store=store))
     return X
 
 
@@ -583,7 +584,9 @@ def plan_search(X_steps, layers, delta: float, w: int, store=None):
     layer's cache is updated once its strategy is chosen.
 
     Returns (plan [T, |M|] int32, loss [T, |M|]: the accepted strategy's loss,
-    or nan where the layer was not compressed)."""
+    or nan where the layer was not compressed).  ``store`` is module_step's
+    storage hook, also applied to the hidden states after each residual add."""
+    keep = store if store is not None else (lambda a: a)
     n_layers = len(layers)
     X0 = np.asarray(X_steps[0], dtype=np.float64)
     B, L, C = X0.shape
@@ -603,7 +606,7 @@ def plan_search(X_steps, layers, delta: float, w: int, store=None):
                 if not _applicable(m, caches[i], B):
                     continue
                 trial = copy.deepcopy(caches[i])
-                Xi = X + module_step(m, X, layers[i], trial, w, store=store)
+                Xi = keep(X + module_step(m, X, layers[i], trial, w, store=store))
                 rest = [ModuleCache() for _ in range(n_layers)]
                 O2 = surrogate_forward(Xi, layers, [FULL] * n_layers, rest, w, first=i + 1, store=store)
                 lv = mrae(O_ref, O2)
@@ -611,7 +614,7 @@ def plan_search(X_steps, layers, delta: float, w: int, store=None):
                     chosen, loss[t, i] = m, lv
                     break
             plan[t, i] = chosen
-            X = X + module_step(chosen, X, layers[i], caches[i], w, store=store)
+            X = keep(X + module_step(chosen, X, layers[i], caches[i], w, store=store))
     return plan, loss
 
 

@@ -124,6 +124,16 @@ dfa_status check_cache(const void* O, const void* Oc, const void* Q, const void*
 
 }  // namespace
 
+int dfa::set_error(int status, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return status;
+}
+
 extern "C" {
 
 const char* dfa_last_error(void) { return g_last_error.c_str(); }

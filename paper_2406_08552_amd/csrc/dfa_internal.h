@@ -33,6 +33,13 @@ struct ProjLaunch {
     int B, H, L, d;
 };
 
+hipError_t launch_mrae(const void* a, const void* b, size_t n, float eps, double* partial, int max_partials,
+                       double* out, hipStream_t stream);
+hipError_t launch_add_bf16(const void* a, const void* b, void* out, size_t n, hipStream_t stream);
+
+// Records the message returned by dfa_last_error() for a non-OK status.
+int set_error(int status, const char* fmt, ...);
+
 bool head_dim_supported(int d);
 bool proj_shape_supported(int H, int d);
 hipError_t launch_qkv_proj(const ProjLaunch& a, hipStream_t stream);

@@ -30,7 +30,8 @@ CODE_NAMES = {FULL: "FULL", WARS_REFRESH: "WARS_REFRESH", WARS_REUSE: "WARS_REUS
 # every symbol include/dfa.h declares
 EXPORTS = ("dfa_attn_full", "dfa_attn_full_and_residual", "dfa_attn_window_plus_residual",
            "dfa_plan_step", "dfa_plan_make", "dfa_qkv_proj", "dfa_out_proj", "dfa_module_step",
-           "dfa_last_error", "dfa_version")
+           "dfa_mrae", "dfa_plan_search_workspace_bytes", "dfa_plan_search", "dfa_last_error", "dfa_version")
+MRAE_WORKSPACE_BYTES = 8192
 
 
 class DfaError(RuntimeError):
@@ -66,6 +67,14 @@ def lib() -> ctypes.CDLL:
         L.dfa_out_proj.restype = _int
         L.dfa_module_step.argtypes = [_int] + [_vp] * 12 + [_int] * 5 + [_vp]
         L.dfa_module_step.restype = _int
+        L.dfa_mrae.argtypes = [_vp, _vp, ctypes.c_size_t, _vp, _vp, _vp]
+        L.dfa_mrae.restype = _int
+        L.dfa_plan_search_workspace_bytes.argtypes = [_int] * 5
+        L.dfa_plan_search_workspace_bytes.restype = ctypes.c_size_t
+        _vpp = ctypes.POINTER(ctypes.c_void_p)
+        L.dfa_plan_search.argtypes = [_int, _int, _vpp, _vpp, _vpp, _vpp, _vpp, ctypes.c_double] + [_int] * 5 + \
+            [_vp, ctypes.c_size_t, _i32p, ctypes.POINTER(ctypes.c_double), _vp]
+        L.dfa_plan_search.restype = _int
         L.dfa_last_error.argtypes = []
         L.dfa_last_error.restype = ctypes.c_char_p
         L.dfa_version.argtypes = []
@@ -204,6 +213,48 @@ def dfa_module_step(code: int, X, Wqkv, bqkv, Wo, bo, Q, K, V, O, R, Y, Ycache, 
     _weights(Wqkv, bqkv, Wo, bo, C)
     _check(lib().dfa_module_step(int(code), _ptr(X), _ptr(Wqkv), _ptr(bqkv), _ptr(Wo), _ptr(bo), _ptr(Q), _ptr(K),
                                  _ptr(V), _ptr(O), _ptr(R), _ptr(Y), _ptr(Ycache), B, H, L, d, w, _stream(stream)))
+
+
+def dfa_mrae(A, B, workspace, result, stream=None) -> None:
+    """result (a 1-element fp64 GPU tensor) = MRAE of two bf16 tensors of the
+    same size; workspace: a uint8 GPU tensor of MRAE_WORKSPACE_BYTES."""
+    import torch
+    if A.dtype != torch.bfloat16 or B.dtype != torch.bfloat16 or A.numel() != B.numel():
+        raise ValueError("A and B must be bf16 tensors of the same size")
+    if not (A.is_contiguous() and B.is_contiguous()):
+        raise ValueError("A and B must be contiguous")
+    if workspace.numel() < MRAE_WORKSPACE_BYTES or result.dtype != torch.float64:
+        raise ValueError("workspace too small or result not fp64")
+    _check(lib().dfa_mrae(_ptr(A), _ptr(B), A.numel(), _ptr(workspace), _ptr(result), _stream(stream)))
+
+
+def plan_search_workspace_bytes(n_layers: int, B: int, H: int, L: int, d: int) -> int:
+    return int(lib().dfa_plan_search_workspace_bytes(n_layers, B, H, L, d))
+
+
+def dfa_plan_search(X_steps, layers, delta: float, w: int, H: int, workspace, stream=None):
+    """Greedy plan search (see include/dfa.h) over hidden states X_steps (list of
+    [B, L, C] bf16 GPU tensors) and layers (list of (Wqkv, bqkv, Wo, bo) GPU
+    tensors); workspace: a uint8 GPU tensor of plan_search_workspace_bytes().
+    Returns (plan int32 [T, n_layers], loss float64 [T, n_layers])."""
+    import torch
+    B, L, C = X_steps[0].shape
+    d = C // H
+    for X in X_steps:
+        _expect(X, torch.bfloat16, (B, L, C), "X_steps[t]")
+    for Wqkv, bqkv, Wo, bo in layers:
+        _weights(Wqkv, bqkv, Wo, bo, C)
+    T, n = len(X_steps), len(layers)
+    arr = lambda ts: (ctypes.c_void_p * len(ts))(*[_ptr(t) for t in ts])  # noqa: E731
+    has_b = all(l[1] is not None for l in layers) and all(l[3] is not None for l in layers)
+    plan = np.full((T, n), -1, dtype=np.int32)
+    loss = np.full((T, n), np.nan)
+    _check(lib().dfa_plan_search(n, T, arr(X_steps), arr([l[0] for l in layers]),
+                                 arr([l[1] for l in layers]) if has_b else None, arr([l[2] for l in layers]),
+                                 arr([l[3] for l in layers]) if has_b else None, float(delta), B, H, L, d, w,
+                                 _ptr(workspace), workspace.numel(), plan.ctypes.data_as(_i32p),
+                                 loss.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), _stream(stream)))
+    return plan, loss
 
 
 def dfa_plan_make(seed: int, n_layers: int, n_steps: int, refresh_every: int, B: int):

@@ -119,6 +119,24 @@ class DriftingX:
         return to_bf16([self.master])[0]
 
 
+def surrogate_states(seed: int, B: int, L: int, C: int, n_steps: int, drift: float, cfg_gap: float = 0.1):
+    """Hidden states [B, L, C] bf16 of a surrogate model over n_steps steps.
+    The conditional half drifts by `drift` per step (DriftingX recipe); the
+    unconditional partner of entry b is entry b plus cfg_gap times an
+    independent drifting draw, so the CFG halves are close but not equal."""
+    cond = DriftingX(seed, 0, (B, L, C), drift)
+    other = DriftingX(seed, 1, (B, L, C), drift)
+    half = B // 2
+    out = []
+    for _ in range(n_steps):
+        a = as_f64(cond.advance())
+        b = as_f64(other.advance())
+        x = a.copy()
+        x[half:] = a[:half] + cfg_gap * b[:half]
+        out.append(torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16))
+    return out
+
+
 def module_weights(seed: int, H: int, d: int):
     """(W_qkv bf16 [3C, C], b_qkv fp32 [3C], W_o bf16 [C, C], b_o fp32 [C]) CPU tensors."""
     C = H * d

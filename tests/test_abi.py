@@ -166,3 +166,26 @@ def test_projection_validation(L):
     assert fm(dfa.FULL, X, W, None, Wo, None, Q, K, V, O, R, Y, Y + 64, *args) == dfa.DFA_ERR_INVALID_ARG
     assert fm(dfa.FULL, X, W, None, Wo, None, Q, K, V, O, R, X, Yc, *args) == dfa.DFA_ERR_INVALID_ARG  # Y == X
     assert fm(dfa.FULL, X, W, None, Wo, None, Q, K, V, O, R, Y, Yc, 2, 16, 64, 72, -1, None) == dfa.DFA_ERR_INVALID_ARG
+
+
+def test_search_and_mrae_validation(L):
+    import ctypes
+    assert L.dfa_mrae(None, 0x1000, 8, 0x2000, 0x3000, None) == dfa.DFA_ERR_INVALID_ARG
+    assert L.dfa_mrae(0x1008, 0x1000, 8, 0x2000, 0x3000, None) == dfa.DFA_ERR_INVALID_ARG   # misaligned
+    assert "aligned" in dfa.last_error()
+    assert dfa.plan_search_workspace_bytes(3, 2, 2, 64, 64) > 0
+    assert dfa.plan_search_workspace_bytes(0, 2, 2, 64, 64) == 0
+    f = L.dfa_plan_search
+    ptrs = (ctypes.c_void_p * 2)(0x100000, 0x200000)
+    plan = np.zeros(4, dtype=np.int32)
+    loss = np.zeros(4)
+    pp = plan.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    lp = loss.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    need = dfa.plan_search_workspace_bytes(2, 2, 2, 64, 64)
+    args = (2, 2, ptrs, ptrs, None, ptrs, None)
+    assert f(*args, -1.0, 2, 2, 64, 64, 8, 0x400000, need, pp, lp, None) == dfa.DFA_ERR_INVALID_ARG   # delta < 0
+    assert f(*args, 0.1, 2, 3, 64, 64, 8, 0x400000, need, pp, lp, None) == dfa.DFA_ERR_UNSUPPORTED    # C = 192
+    assert f(*args, 0.1, 2, 2, 64, 64, 8, 0x400000, need - 1, pp, lp, None) == dfa.DFA_ERR_INVALID_ARG
+    assert "too small" in dfa.last_error()
+    assert f(*args, 0.1, 2, 2, 64, 64, 8, 0x400010, need, pp, lp, None) == dfa.DFA_ERR_INVALID_ARG
+    assert f(*args, 0.1, 2, 2, 64, 64, 8, 0x400000, need, None, lp, None) == dfa.DFA_ERR_INVALID_ARG

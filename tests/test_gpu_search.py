@@ -1,0 +1,110 @@
+"""GPU parity of the MRAE loss and of the greedy plan search (Sec. 3.5, Alg. 1)
+against the fp64 oracle, through the C ABI.
+
+MRAE: relative tolerance 1e-5 (each lane sums in fp32, partial sums in fp64).
+Plan search: the plan is a sequence of integer decisions, each taken by
+comparing a loss with a threshold, and the library computes its losses on
+bf16 activations while the oracle computes them in fp64.  The test therefore
+compares against the oracle run with the library's storage precision (Q, K,
+V, O and the hidden states rounded to bf16 where the library stores them),
+and first checks that the case is well posed: the oracle's plan must not
+change when delta moves by 3% either way, so no decision sits within 3% of
+its threshold.  Then the GPU plan must equal the oracle plan exactly, and the
+accepted losses must agree to 5% (relative) or n_layers * 2^-8 (absolute).
+The absolute part: a compressed path may use another kernel than the
+reference path (ASC's conditional half runs the full-attention kernel, the
+uncompressed reference the refresh kernel), and their bf16 outputs can differ
+by one ulp per element; the loss counts a one-ulp difference as 2^-8, and
+such differences can arise at every layer.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import dfa_oracle as orc
+from paper_2406_08552_amd import dfa, inputs
+from tests.test_gpu_parity import say
+
+pytestmark = pytest.mark.gpu
+f64 = inputs.as_f64
+
+
+def to_bf16_f64(a):
+    return f64(torch.from_numpy(np.ascontiguousarray(a)).to(torch.bfloat16))
+
+
+@pytest.mark.parametrize("n", [1, 7, 8, 1000, 12345, 1 << 20, 3 << 20])
+def test_mrae_vs_oracle(n):
+    dev = torch.device("cuda")
+    g = torch.Generator().manual_seed(n)
+    a = torch.randn(n, generator=g).to(torch.bfloat16)
+    b = (a.float() + 0.3 * torch.randn(n, generator=g)).to(torch.bfloat16)
+    if n > 16:
+        b[: n // 8] = a[: n // 8]            # equal pairs
+        a[n // 8: n // 4] = 0                # zero against nonzero
+        b[n // 4: n // 4 + 5] = 0
+        a[n // 4: n // 4 + 5] = 0            # zero pairs
+        b[n // 2: n // 2 + n // 10] = -a[n // 2: n // 2 + n // 10]   # sign flips
+    ws = torch.empty(dfa.MRAE_WORKSPACE_BYTES, dtype=torch.uint8, device=dev)
+    out = torch.zeros(2, dtype=torch.float64, device=dev)
+    ga, gb = a.to(dev), b.to(dev)
+    say(f"mrae n={n}")
+    dfa.dfa_mrae(ga, gb, ws, out[0:1])
+    dfa.dfa_mrae(ga, gb, ws, out[1:2])
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    ref = orc.mrae(f64(a), f64(b))
+    assert got[0] == got[1], "MRAE must be deterministic"
+    assert abs(got[0] - ref) <= 1e-5 * ref + 1e-12, (got[0], ref)
+
+
+def _surrogate(dev, B, L, H, d, n_layers, T, drift, seed=21):
+    C = H * d
+    Xs = inputs.surrogate_states(seed, B, L, C, T, drift)
+    layers_cpu = [inputs.module_weights(100 + i, H, d) for i in range(n_layers)]
+    layers_gpu = [tuple(t.to(dev) for t in lw) for lw in layers_cpu]
+    layers_orc = [orc.ModuleWeights(*(f64(t) for t in lw), H) for lw in layers_cpu]
+    return Xs, [x.to(dev) for x in Xs], layers_gpu, layers_orc
+
+
+def _search_gpu(Xg, layers_gpu, delta, w, H):
+    B, L, C = Xg[0].shape
+    ws = torch.empty(dfa.plan_search_workspace_bytes(len(layers_gpu), B, H, L, C // H), dtype=torch.uint8,
+                     device=Xg[0].device)
+    return dfa.dfa_plan_search(Xg, layers_gpu, delta, w, H, ws)
+
+
+def test_search_degenerate_cases():
+    dev = torch.device("cuda")
+    B, L, H, d, n, T, w = 2, 64, 2, 64, 3, 3, 8
+    Xs, Xg, lg, _ = _surrogate(dev, B, L, H, d, n, T, 0.02)
+    say("search delta=0")
+    plan, loss = _search_gpu(Xg, lg, 0.0, w, H)
+    assert np.all(plan == dfa.WARS_REFRESH) and np.all(np.isnan(loss))
+    say("search delta=inf")
+    plan, _ = _search_gpu(Xg, lg, 1e30, w, H)
+    assert np.all(plan[0] == dfa.ASC_REUSE) and np.all(plan[1:] == dfa.AST_REUSE)
+    say("search zero drift")
+    plan, loss = _search_gpu([Xg[0]] * 3, lg, 1e-9, w, H)
+    assert np.all(plan[0] == dfa.WARS_REFRESH) and np.all(plan[1:] == dfa.AST_REUSE)
+    assert np.all(loss[1:] == 0.0), "AST of an unchanged input must reproduce the reference exactly"
+
+
+@pytest.mark.parametrize("drift,w,delta", [(0.08, 48, 0.09), (0.01, 16, 0.05), (0.05, 40, 0.2)])
+def test_search_vs_oracle(drift, w, delta):
+    dev = torch.device("cuda")
+    B, L, H, d, n, T = 2, 64, 2, 64, 3, 5
+    Xs, Xg, lg, lo = _surrogate(dev, B, L, H, d, n, T, drift)
+    Xd = [f64(x) for x in Xs]
+    ref, ref_loss = orc.plan_search(Xd, lo, delta, w, store=to_bf16_f64)
+    for scale in (0.97, 1.03):
+        other, _ = orc.plan_search(Xd, lo, delta * scale, w, store=to_bf16_f64)
+        assert np.array_equal(other, ref), "ill-posed case: a decision lies within 3% of its threshold"
+    say(f"search drift={drift} w={w} delta={delta}")
+    plan, loss = _search_gpu(Xg, lg, delta, w, H)
+    say(f"plan {plan.tolist()} oracle {ref.tolist()}")
+    assert np.array_equal(plan, ref), (plan.tolist(), ref.tolist())
+    both = ~np.isnan(ref_loss)
+    assert np.array_equal(both, ~np.isnan(loss))
+    assert np.all(np.abs(loss[both] - ref_loss[both]) <= np.maximum(0.05 * ref_loss[both], n * 2.0 ** -8)), \
+        (loss.tolist(), ref_loss.tolist())
