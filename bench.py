@@ -86,6 +86,34 @@ def timed(torch, stream, fn, reps):
     return s0.elapsed_time(s1) / reps
 
 
+def video_bench(args, dfa, inputs, torch, dev, stream):
+    """Attention kernels at the Open-Sora V1.1 240p 16-frame shapes: spatial
+    attention within frames (32 sequences of 405 tokens per head) and
+    temporal attention across frames (810 sequences of 16)."""
+    out = {}
+    for key in ("opensora_spatial", "opensora_temporal"):
+        cfg = inputs.CONFIGS[key]
+        B, H, L, d, w = cfg.B, cfg.H, cfg.L, cfg.d, cfg.w
+        shape = (B, H, L, d)
+        q, k, v = inputs.device_qkv(inputs.SEED_BASE + 7000 + cfg.cfg_id, shape, dev)
+        O = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+        R = torch.empty(shape, dtype=torch.float32, device=dev)
+        full = 4.0 * B * H * L * L * d
+        band = 4.0 * B * H * d * n_band(L, w)
+        runs = {
+            "full": (lambda: dfa.dfa_attn_full(q, k, v, O, w, stream), full),
+            "wars_refresh": (lambda: dfa.dfa_attn_full_and_residual(q, k, v, O, R, w, stream), full),
+            "wars_reuse": (lambda: dfa.dfa_attn_window_plus_residual(q, k, v, O, R, w, stream), band),
+            "asc": (lambda: dfa.dfa_plan_step(dfa.ASC_REUSE, q, k, v, O, None, None, w, stream), full / 2),
+        }
+        res = {"B": B, "L": L, "w": w}
+        for name, (fn, fl) in runs.items():
+            ms = timed(torch, stream, fn, args.kernel_reps)
+            res[name] = {"ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 1)}
+        out[cfg.name] = res
+    return out
+
+
 def search_bench(args, dfa, inputs, torch, dev, stream):
     """The greedy plan search (Alg. 1) on a 28-layer surrogate of DiT-XL/2 at
     512 px (B = 8 as four CFG pairs, L = 1024, H = 16, d = 72, band half-width
@@ -343,6 +371,7 @@ def main():
                       "gbs": round(ntens * tensor_bytes / (ms * 1e-3) / 1e9, 1)}
 
     module = module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres)
+    video = video_bench(args, dfa, inputs, torch, dev, stream)
 
     full_ms = sum(per_code.get(0, [])) / max(1, len(per_code.get(0, [])))
     full_flops = code_flops(0, B, H, L, d, w)
@@ -380,6 +409,7 @@ def main():
         "full_equiv_tflops": round(plan_layer_steps * full_flops / (ms_per_step * 1e-3) / 1e12, 1),
         "kernels": kres,
         "module": module,
+        "video": video,
         "reuse_speedup_vs_full": round(kres["full"]["ms"] / kres["wars_reuse"]["ms"], 3),
         "reuse_ideal_speedup": round(L * L / n_band(L, w), 3),
         "roofline": {"kernel": "attn_kernel<72, FULL> (dfa_attn_full / FULL plan entries)", "bound": "mfma",

@@ -64,6 +64,15 @@ CONFIGS = {
                            n_layers=28, n_steps=20, refresh_every=4),
     "pixart2k": AttnConfig("pixart_sigma_2048px", 5, B=2, H=16, L=16384, d=72, w=2048,
                            n_layers=28, n_steps=20, refresh_every=4),
+    # Open-Sora V1.1 at 240p with 16 frames (STDiT: hidden 1152 = 16 heads x 72).
+    # The paper gives no attention shapes; read here as 240 x 426 frames, an 8x
+    # VAE and 2 x 2 patches: 15 x 27 = 405 tokens per frame.  Spatial attention
+    # runs within each frame (batch = CFG pair x 16 frames, CFG-major), temporal
+    # attention across the 16 frames of each token (batch = CFG pair x 405).
+    "opensora_spatial": AttnConfig("opensora_v1.1_240p_16f_spatial", 6, B=32, H=16, L=405, d=72, w=50,
+                                   n_layers=28, n_steps=20, refresh_every=0),
+    "opensora_temporal": AttnConfig("opensora_v1.1_240p_16f_temporal", 7, B=810, H=16, L=16, d=72, w=2,
+                                    n_layers=28, n_steps=20, refresh_every=0),
 }
 
 

@@ -40,17 +40,17 @@ def bf16_floor(ref):
     return float(e.mean()), float(e.max())
 
 
-def check(name, got, ref, rows=None):
+def check(name, got, ref, rows=None, max_abs=MAX_ABS):
     g = f64(got)
     if rows is not None:
         g = g[:, :, rows]
     err = np.abs(g - ref)
     assert np.all(np.isfinite(g)), f"{name}: non-finite output"
     mx, mn = float(err.max()), float(err.mean())
-    mean_bar, max_bar = MEAN_ABS, MAX_ABS
+    mean_bar, max_bar = MEAN_ABS, max_abs
     if got.dtype == torch.bfloat16:
         fmean, fmax = bf16_floor(ref)
-        mean_bar, max_bar = max(MEAN_ABS, 1.1 * fmean), max(MAX_ABS, 1.25 * fmax)
+        mean_bar, max_bar = max(MEAN_ABS, 1.1 * fmean), max(max_abs, 1.25 * fmax)
     assert mx <= max_bar and mn <= mean_bar, \
         f"{name}: max abs {mx:.3e} (bar {max_bar:.3e}), mean abs {mn:.3e} (bar {mean_bar:.3e})"
     return mx, mn
@@ -195,7 +195,7 @@ MIXED_CODES = [dfa.WARS_REFRESH, dfa.WARS_REUSE, dfa.WARS_ASC_REUSE, dfa.AST_REU
                dfa.WARS_ASC_REUSE]
 
 
-def run_plan(cfg_key, layers, n_steps, n_rows=None, alias_cache=(), codes=None):
+def run_plan(cfg_key, layers, n_steps, n_rows=None, alias_cache=(), codes=None, few_keys=False):
     cfg = inputs.CONFIGS[cfg_key]
     dev = torch.device("cuda")
     shape = (cfg.B, cfg.H, cfg.L, cfg.d)
@@ -235,11 +235,16 @@ def run_plan(cfg_key, layers, n_steps, n_rows=None, alias_cache=(), codes=None):
             else:
                 ref = orc.plan_step_rows(c, Qd, Kd, Vd, rows, cache, cfg.w)
             got = O.cpu()
-            check(f"{cfg_key} l{layer} t{t} O", got, ref, rows)
+            # With few keys per query the bf16 rounding of the probabilities
+            # does not average out: it moves an output by at most
+            # 2^-8 * sum_j p_j |v_j| <= 2^-8 * max |V| (PV and the row sum use
+            # the same rounded probabilities), on top of the output rounding.
+            mbar = max(MAX_ABS, 2.0 ** -8 * float(np.abs(Vd).max()) + 2.0 ** -8) if few_keys else MAX_ABS
+            check(f"{cfg_key} l{layer} t{t} O", got, ref, rows, mbar)
             if c == dfa.WARS_REFRESH:
-                check(f"{cfg_key} l{layer} t{t} R", R, cache.R, rows)
+                check(f"{cfg_key} l{layer} t{t} R", R, cache.R, rows, mbar)
             if c == dfa.WARS_ASC_REFRESH:
-                check(f"{cfg_key} l{layer} t{t} R[cond]", R[:half], cache.R, rows)
+                check(f"{cfg_key} l{layer} t{t} R[cond]", R[:half], cache.R, rows, mbar)
                 assert torch.equal(R[half:].cpu(), R_before[half:]), "a half-batch refresh must leave R[uncond]"
             if c == dfa.AST_REUSE:
                 assert torch.equal(got, outputs[int(o_src[t, layer])]), "AST must return the cached step bitwise"
@@ -347,3 +352,11 @@ def test_checkpoint_resume_bit_exact():
         outs = run(k, len(MIXED_CODES), O2, R2, Oc2)
         for t, got in zip(range(k, len(MIXED_CODES)), outs):
             assert torch.equal(got, ref[t]), f"resumed run differs at step {t} ({dfa.CODE_NAMES[MIXED_CODES[t]]})"
+
+
+@pytest.mark.parametrize("key,n_rows", [("opensora_spatial", 64), ("opensora_temporal", None)])
+def test_video_shapes(key, n_rows):
+    """Open-Sora-shaped spatial (405 tokens per frame) and temporal (16
+    frames) attention through every plan code, CFG pairs batch-major."""
+    run_plan(key, layers=[0], n_steps=len(MIXED_CODES), n_rows=n_rows, codes=MIXED_CODES,
+             few_keys=key == "opensora_temporal")
