@@ -8,22 +8,34 @@
 //        QKV projection, or the attention output O [B][H][L][d] read as the
 //        [M][H * d] matrix of merged heads for the output projection
 //   D    [N][M]  one output feature per row, one token per column
-// The QKV epilogue adds the bias and scatters each group of four features
-// straight into Q, K and V in the [B][H][L][d] layout of the attention
-// kernels (feature f = which * C + head * d + dim); the output-projection
-// epilogue adds the bias and stores token-major Y [M][N] to every
-// destination given (the unconditional half of an ASC step is one of them).
+// The epilogue adds the bias, rounds to bf16 and passes the output tile
+// through LDS as [token][feature] rows, so that it leaves as 16-byte chunks
+// in row order: the QKV projection scatters each chunk of eight features
+// straight into Q, K or V in the [B][H][L][d] layout of the attention kernels
+// (feature f = which * C + head * d + dim, and d is a multiple of 8, so a
+// chunk never straddles a head); the output projection stores token-major
+// Y [M][N] to every destination given (the unconditional half of an ASC step
+// is one of them).
 //
 // Work decomposition: a workgroup (4 wavefronts) owns 128 features x 128
-// tokens and walks K in tiles of 64, staged in LDS by direct global->LDS
-// copies with double buffering.  Each wavefront owns 64 x 64 outputs as 2 x 2
-// blocks of v_mfma_f32_32x32x16_bf16 (operand layouts: lane l, h = l / 32,
-// A element e = A[l % 32][8h + e], B element e = B[8h + e][l % 32], output
-// element i = D[8 (i/4) + 4h + i%4][l % 32]).  LDS rows have a 144-byte
-// pitch, so the 16-byte operand reads of 16 consecutive rows hit distinct
-// bank groups.  Blocks are remapped so that each XCD works through a
-// contiguous range of token tiles with all their feature tiles, keeping the
-// token tile's activations in that XCD's L2.
+// tokens and walks K in tiles of 64.  The next k-tile is loaded from global
+// memory into registers while the MFMAs consume the current one from LDS,
+// then stored into the other LDS buffer (double buffering, one barrier per
+// k-tile).  Each wavefront owns 64 x 64 outputs as 2 x 2 blocks of
+// v_mfma_f32_32x32x16_bf16 (operand layouts: lane l, h = l / 32, A element
+// e = A[l % 32][8h + e], B element e = B[8h + e][l % 32], output element
+// i = D[8 (i/4) + 4h + i%4][l % 32]).  LDS rows have a 144-byte pitch, so the
+// 16-byte operand reads of 16 consecutive rows hit distinct bank groups.
+// Blocks are remapped so that each XCD works through a contiguous range of
+// token tiles with all their feature tiles, keeping the token tile's
+// activations in that XCD's L2.
+//
+// Measured at 32768 tokens x 1152 features (PixArt-Sigma at 2048 px), against
+// earlier forms of this kernel: scattering 8-byte pieces straight from the
+// accumulators cost about a quarter of the QKV projection's time, and direct
+// global->LDS copies were no faster than register staging here.  Larger
+// workgroup tiles (192 x 256, one wavefront per SIMD, also with a four-stage
+// copy ring) did not beat this shape.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -47,7 +59,7 @@ constexpr int GPC = 9;                           // row pitch in 16-byte chunks 
 constexpr int GP = GPC * 8;                      // row pitch in elements
 constexpr int G_TILE = 128 * GP;                 // one operand tile (128 rows)
 constexpr int G_STAGE = 2 * G_TILE;              // A tile, then B tile
-constexpr int G_ROUNDS = (128 * GPC + GT - 1) / GT;
+constexpr int G_OP = GF + 8;                     // output staging row pitch (elements)
 
 enum { ACT_ROWS = 0, ACT_HEADS = 1 };   // activations: [M][K] rows, or O [B][H][L][d]
 enum { OUT_QKV = 0, OUT_ROWS = 1 };     // epilogue: scatter to Q/K/V, or [M][N] rows
@@ -68,36 +80,43 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, bf16x2{(__bf16)lo, (__bf16)hi});
 }
 
-__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
-
-// Direct global -> LDS copy of the W and activation tiles of k-tile kt.
-// Token rows beyond M copy row M - 1 (their outputs are not stored).
+// Global -> register loads of k-tile kt: thread tid owns chunks
+// c = it * GT + tid of the W tile (it < 4) and of the activation tile
+// (it >= 4), chunk c being row c / 8, 16-byte column c % 8.  Token rows
+// beyond M load row M - 1 (their outputs are not stored).
 template <int ACT>
-__device__ __forceinline__ void issue_gemm_tile(const GemmParams& p, int n0, int t0, int kt, int tid, uint16_t* As,
-                                                uint16_t* Bs) {
-    const int wave_chunk0 = tid & ~63;
+__device__ __forceinline__ void load_gemm_tile(const GemmParams& p, int n0, int t0, int kt, int tid, u32x4 (&r)[8]) {
 #pragma unroll
-    for (int it = 0; it < G_ROUNDS; ++it) {
+    for (int it = 0; it < 4; ++it) {
         const int c = it * GT + tid;
-        const int row = c / GPC, ch = c % GPC;
-        if (row < 128 && ch < 8) {
-            const int kk = kt * GK + ch * 8;
-            __builtin_amdgcn_global_load_lds((const void*)(p.W + (size_t)(n0 + row) * p.K + kk),
-                                             (__attribute__((address_space(3))) void*)(As + (it * GT + wave_chunk0) * 8),
-                                             16, 0, 0);
-            const int t = min(t0 + row, p.M - 1);
-            const uint16_t* src;
-            if constexpr (ACT == ACT_ROWS) {
-                src = p.act + (size_t)t * p.K + kk;
-            } else {
-                const int b = t / p.L, l = t - b * p.L;
-                const int h = kk / p.d, j = kk - h * p.d;
-                src = p.act + ((size_t)(b * p.H + h) * p.L + l) * p.d + j;
-            }
-            __builtin_amdgcn_global_load_lds((const void*)src,
-                                             (__attribute__((address_space(3))) void*)(Bs + (it * GT + wave_chunk0) * 8),
-                                             16, 0, 0);
+        const int row = c >> 3, ch = c & 7;
+        r[it] = *(const u32x4*)(p.W + (size_t)(n0 + row) * p.K + kt * GK + ch * 8);
+    }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int c = it * GT + tid;
+        const int row = c >> 3, ch = c & 7;
+        const int kk = kt * GK + ch * 8;
+        const int t = min(t0 + row, p.M - 1);
+        const uint16_t* src;
+        if constexpr (ACT == ACT_ROWS) {
+            src = p.act + (size_t)t * p.K + kk;
+        } else {
+            const int b = t / p.L, l = t - b * p.L;
+            const int h = kk / p.d, j = kk - h * p.d;
+            src = p.act + ((size_t)(b * p.H + h) * p.L + l) * p.d + j;
         }
+        r[4 + it] = *(const u32x4*)src;
+    }
+}
+
+__device__ __forceinline__ void store_gemm_tile(int tid, const u32x4 (&r)[8], uint16_t* As, uint16_t* Bs) {
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int c = it * GT + tid;
+        const int row = c >> 3, ch = c & 7;
+        *(u32x4*)(As + row * GP + ch * 8) = r[it];
+        *(u32x4*)(Bs + row * GP + ch * 8) = r[4 + it];
     }
 }
 
@@ -125,16 +144,14 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 
     const int nk = p.K / GK;
     int stage = 0;
-    issue_gemm_tile<ACT>(p, n0, t0, 0, tid, smem, smem + G_TILE);
-    wait_vm_all();
+    u32x4 stg[8];
+    load_gemm_tile<ACT>(p, n0, t0, 0, tid, stg);
+    store_gemm_tile(tid, stg, smem, smem + G_TILE);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
         const uint16_t* As = smem + stage * G_STAGE;
         const uint16_t* Bs = As + G_TILE;
-        if (kt + 1 < nk) {
-            uint16_t* An = smem + (stage ^ 1) * G_STAGE;
-            issue_gemm_tile<ACT>(p, n0, t0, kt + 1, tid, An, An + G_TILE);
-        }
+        if (kt + 1 < nk) load_gemm_tile<ACT>(p, n0, t0, kt + 1, tid, stg);
         const uint16_t* arow = As + (64 * wf + r32) * GP + 8 * h;
         const uint16_t* brow = Bs + (64 * wt + r32) * GP + 8 * h;
 #pragma unroll
@@ -150,34 +167,49 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
                 for (int nb = 0; nb < 2; ++nb)
                     acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mb], b[nb], acc[mb][nb], 0, 0, 0);
         }
-        wait_vm_all();
+        if (kt + 1 < nk) {
+            uint16_t* An = smem + (stage ^ 1) * G_STAGE;
+            store_gemm_tile(tid, stg, An, An + G_TILE);
+        }
         __syncthreads();
         stage ^= 1;
     }
 
-    // epilogue: bias, bf16, store (four consecutive features per group)
-    const int C = p.N / 3;
+    // epilogue: bias and bf16 rounding, then the tile goes through LDS as
+    // [token][feature] rows so that the stores are 16-byte chunks in row
+    // order (the loop ended on a barrier, so every stage is free)
+    uint16_t* ot = smem;
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
-        const int t = t0 + 64 * wt + 32 * nb + r32;
-        if (t >= p.M) continue;
-        const int b = t / p.L, l = t - b * p.L;
+        const int tl = 64 * wt + 32 * nb + r32;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb) {
 #pragma unroll
             for (int jb = 0; jb < 4; ++jb) {
-                const int f = n0 + 64 * wf + 32 * mb + 8 * jb + 4 * h;
+                const int fl = 64 * wf + 32 * mb + 8 * jb + 4 * h;
                 f32x4 v{acc[mb][nb][4 * jb], acc[mb][nb][4 * jb + 1], acc[mb][nb][4 * jb + 2], acc[mb][nb][4 * jb + 3]};
-                if (p.bias) v += *(const f32x4*)(p.bias + f);
-                const u32x2 ov = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
-                if constexpr (OUT == OUT_QKV) {
-                    const int which = f / C, rem = f - which * C;
-                    const int head = rem / p.d, dim = rem - head * p.d;
-                    *(u32x2*)(p.dst[which] + ((size_t)(b * p.H + head) * p.L + l) * p.d + dim) = ov;
-                } else {
-                    for (int di = 0; di < p.ndst; ++di) *(u32x2*)(p.dst[di] + (size_t)t * p.N + f) = ov;
-                }
+                if (p.bias) v += *(const f32x4*)(p.bias + n0 + fl);
+                *(u32x2*)(ot + tl * G_OP + fl) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
             }
+        }
+    }
+    __syncthreads();
+    const int C = p.N / 3;
+#pragma unroll
+    for (int it = 0; it < GTOK * GF / 8 / GT; ++it) {
+        const int c = it * GT + tid;
+        const int tl = c / (GF / 8), g = c % (GF / 8);
+        const int t = t0 + tl;
+        if (t >= p.M) continue;
+        const u32x4 val = *(const u32x4*)(ot + tl * G_OP + 8 * g);
+        const int f = n0 + 8 * g;
+        if constexpr (OUT == OUT_QKV) {
+            const int b = t / p.L, l = t - b * p.L;
+            const int which = f / C, rem = f - which * C;
+            const int head = rem / p.d, dim = rem - head * p.d;
+            *(u32x4*)(p.dst[which] + ((size_t)(b * p.H + head) * p.L + l) * p.d + dim) = val;
+        } else {
+            for (int di = 0; di < p.ndst; ++di) *(u32x4*)(p.dst[di] + (size_t)t * p.N + f) = val;
         }
     }
 }
