@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG_DIR, "libdfa.so")
 
-SOURCES = ["dfa_kernels.hip", "dfa_gemm.hip", "dfa_reduce.hip", "dfa_api.cpp", "dfa_search.cpp"]
+SOURCES = ["dfa_kernels.hip", "dfa_short.hip", "dfa_gemm.hip", "dfa_reduce.hip", "dfa_api.cpp", "dfa_search.cpp"]
 ARCH = "gfx950"
 # Packed fp32 VALU forms are kept out of the device code; the host pass only
 # warns that it does not know the feature.

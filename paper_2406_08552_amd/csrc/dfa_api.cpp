@@ -152,7 +152,7 @@ dfa_status dfa_attn_full(const void* Q, const void* K, const void* V, void* O, v
     dfa::AttnLaunch a = make_launch(Q, K, V, s);
     a.dst[0] = O;
     a.ndst = 1;
-    return hip_status(dfa::launch_full(a, stream), "dfa_attn_full launch");
+    return hip_status(dfa::attn_full(a, stream), "dfa_attn_full launch");
 }
 
 dfa_status dfa_attn_full_and_residual(const void* Q, const void* K, const void* V, void* O, void* R, int B, int H,
@@ -170,7 +170,7 @@ dfa_status dfa_attn_full_and_residual(const void* Q, const void* K, const void* 
     a.dst[0] = O;
     a.ndst = 1;
     a.Rout = R;
-    return hip_status(dfa::launch_refresh(a, stream), "dfa_attn_full_and_residual launch");
+    return hip_status(dfa::attn_refresh(a, stream), "dfa_attn_full_and_residual launch");
 }
 
 dfa_status dfa_attn_window_plus_residual(const void* Q, const void* K, const void* V, void* O, const void* R, int B,
@@ -187,7 +187,7 @@ dfa_status dfa_attn_window_plus_residual(const void* Q, const void* K, const voi
     a.dst[0] = O;
     a.ndst = 1;
     a.Rin = R;
-    return hip_status(dfa::launch_window(a, stream), "dfa_attn_window_plus_residual launch");
+    return hip_status(dfa::attn_window(a, stream), "dfa_attn_window_plus_residual launch");
 }
 
 dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, void* O, void* R, void* Ocache,
@@ -240,16 +240,16 @@ dfa_status dfa_plan_step(int code, const void* Q, const void* K, const void* V, 
     }
     switch (code) {
         case DFA_FULL:
-            return hip_status(dfa::launch_full(a, stream), "FULL launch");
+            return hip_status(dfa::attn_full(a, stream), "FULL launch");
         case DFA_ASC_REUSE:
-            return hip_status(dfa::launch_asc(a, stream), "ASC launch");
+            return hip_status(dfa::attn_asc(a, stream), "ASC launch");
         case DFA_WARS_REFRESH:
         case DFA_WARS_ASC_REFRESH:
             a.Rout = R;
-            return hip_status(dfa::launch_refresh(a, stream), "WA-RS refresh launch");
+            return hip_status(dfa::attn_refresh(a, stream), "WA-RS refresh launch");
         default:  // DFA_WARS_REUSE, DFA_WARS_ASC_REUSE
             a.Rin = R;
-            return hip_status(dfa::launch_window(a, stream), "WA-RS reuse launch");
+            return hip_status(dfa::attn_window(a, stream), "WA-RS reuse launch");
     }
 }
 
@@ -420,16 +420,16 @@ dfa_status dfa_module_step(int code, const void* X, const void* Wqkv, const void
     switch (code) {
         case DFA_FULL:
         case DFA_ASC_REUSE:
-            e = dfa::launch_full(a, stream);
+            e = dfa::attn_full(a, stream);
             break;
         case DFA_WARS_REFRESH:
         case DFA_WARS_ASC_REFRESH:
             a.Rout = R;
-            e = dfa::launch_refresh(a, stream);
+            e = dfa::attn_refresh(a, stream);
             break;
         default:  // DFA_WARS_REUSE, DFA_WARS_ASC_REUSE
             a.Rin = R;
-            e = dfa::launch_window(a, stream);
+            e = dfa::attn_window(a, stream);
             break;
     }
     if ((st = hip_status(e, "module attention launch")) != DFA_OK) return st;

@@ -50,6 +50,28 @@ hipError_t launch_refresh(const AttnLaunch& a, hipStream_t stream);
 hipError_t launch_window(const AttnLaunch& a, hipStream_t stream);
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t stream);
 
+// One-wavefront-per-sequence kernels for L <= SHORT_L_MAX (dfa_short.hip).
+constexpr int SHORT_L_MAX = 32;
+hipError_t launch_short_full(const AttnLaunch& a, hipStream_t stream);
+hipError_t launch_short_asc(const AttnLaunch& a, hipStream_t stream);
+hipError_t launch_short_refresh(const AttnLaunch& a, hipStream_t stream);
+hipError_t launch_short_window(const AttnLaunch& a, hipStream_t stream);
+
+// The attention operations: short sequences take the per-sequence kernels,
+// longer ones the tiled kernels.
+inline hipError_t attn_full(const AttnLaunch& a, hipStream_t s) {
+    return a.L <= SHORT_L_MAX ? launch_short_full(a, s) : launch_full(a, s);
+}
+inline hipError_t attn_asc(const AttnLaunch& a, hipStream_t s) {
+    return a.L <= SHORT_L_MAX ? launch_short_asc(a, s) : launch_asc(a, s);
+}
+inline hipError_t attn_refresh(const AttnLaunch& a, hipStream_t s) {
+    return a.L <= SHORT_L_MAX ? launch_short_refresh(a, s) : launch_refresh(a, s);
+}
+inline hipError_t attn_window(const AttnLaunch& a, hipStream_t s) {
+    return a.L <= SHORT_L_MAX ? launch_short_window(a, s) : launch_window(a, s);
+}
+
 }  // namespace dfa
 
 #endif

@@ -86,6 +86,15 @@ SHAPES = [  # (B, H, L, d, w): tiles, ragged tails, degenerate bands
     (1, 1, 129, 64, 1000),
     (1, 1, 513, 72, 1),
     (3, 1, 384, 72, 64),
+    # short sequences (one wavefront per sequence): B*H not a multiple of the
+    # four sequences of a workgroup, one and two 16-key blocks, bands covering
+    # every key, and the first length that takes the tiled kernels again
+    (3, 5, 16, 72, 2),
+    (2, 3, 32, 72, 31),
+    (1, 2, 31, 72, 4),
+    (2, 2, 12, 64, 0),
+    (1, 3, 25, 64, 30),
+    (1, 1, 33, 72, 3),
 ]
 
 
@@ -289,7 +298,8 @@ def test_plan_mixed_codes_pixart2k_sampled():
 def test_wars_asc_odd_shapes():
     """WA-RS + ASC on ragged tiles and degenerate bands (B = 4: two CFG pairs)."""
     dev = torch.device("cuda")
-    for (B, H, L, d, w) in ((4, 1, 77, 72, 5), (2, 2, 129, 64, 0), (4, 2, 300, 72, 299), (2, 1, 1, 72, 0)):
+    for (B, H, L, d, w) in ((4, 1, 77, 72, 5), (2, 2, 129, 64, 0), (4, 2, 300, 72, 299), (2, 1, 1, 72, 0),
+                            (4, 3, 16, 72, 2), (2, 1, 29, 64, 28)):
         shape = (B, H, L, d)
         say(f"wars+asc B={B} H={H} L={L} d={d} w={w}")
         q0, k0, v0 = rand_qkv(shape, 300 + L + w)
