@@ -18,24 +18,26 @@
 // is one of them).
 //
 // Work decomposition: a workgroup (4 wavefronts) owns 128 features x 128
-// tokens and walks K in tiles of 64.  The next k-tile is loaded from global
-// memory into registers while the MFMAs consume the current one from LDS,
-// then stored into the other LDS buffer (double buffering, one barrier per
-// k-tile).  Each wavefront owns 64 x 64 outputs as 2 x 2 blocks of
-// v_mfma_f32_32x32x16_bf16 (operand layouts: lane l, h = l / 32, A element
+// or 256 tokens (the larger tile when the grid still has four rounds of work
+// per CU) and walks K in tiles of 64 or 32.  The next k-tile is loaded from
+// global memory into registers while the MFMAs consume the current one from
+// LDS, then stored into the other LDS buffer (double buffering, one barrier
+// per k-tile).  Each wavefront owns 64 features x 64 or 128 tokens as blocks
+// of v_mfma_f32_32x32x16_bf16 (operand layouts: lane l, h = l / 32, A element
 // e = A[l % 32][8h + e], B element e = B[8h + e][l % 32], output element
-// i = D[8 (i/4) + 4h + i%4][l % 32]).  LDS rows have a 144-byte pitch, so the
-// 16-byte operand reads of 16 consecutive rows hit distinct bank groups.
-// Blocks are remapped so that each XCD works through a contiguous range of
-// token tiles with all their feature tiles, keeping the token tile's
-// activations in that XCD's L2.
+// i = D[8 (i/4) + 4h + i%4][l % 32]).  LDS rows carry one 16-byte pad chunk
+// (144- or 80-byte pitch), so the 16-byte operand reads of 16 consecutive rows
+// hit distinct bank groups.  Blocks are remapped so that each XCD works
+// through a contiguous range of token tiles with all their feature tiles,
+// keeping the token tile's activations in that XCD's L2.
 //
 // Measured at 32768 tokens x 1152 features (PixArt-Sigma at 2048 px), against
 // earlier forms of this kernel: scattering 8-byte pieces straight from the
-// accumulators cost about a quarter of the QKV projection's time, and direct
-// global->LDS copies were no faster than register staging here.  Larger
-// workgroup tiles (192 x 256, one wavefront per SIMD, also with a four-stage
-// copy ring) did not beat this shape.
+// accumulators cost about a quarter of the QKV projection's time; direct
+// global->LDS copies were no faster than register staging; the 256-token
+// tile takes about 10% off the QKV projection.  Larger tiles still
+// (192 x 256 at one wavefront per SIMD, also with a four-stage copy ring)
+// did not beat these shapes.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -53,13 +55,28 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int GT = 256;                          // threads per workgroup
 constexpr int GF = 128;                          // features per workgroup
-constexpr int GTOK = 128;                        // tokens per workgroup
-constexpr int GK = 64;                           // k per LDS tile
-constexpr int GPC = 9;                           // row pitch in 16-byte chunks (8 data + 1 pad)
-constexpr int GP = GPC * 8;                      // row pitch in elements
-constexpr int G_TILE = 128 * GP;                 // one operand tile (128 rows)
-constexpr int G_STAGE = 2 * G_TILE;              // A tile, then B tile
-constexpr int G_OP = GF + 8;                     // output staging row pitch (elements)
+constexpr int TILE_FEW = 0, TILE_MANY = 1;       // workgroup tile shapes (see Tile)
+
+// Workgroup tile shape.  TILE_FEW: 128 tokens, k-tiles of 64 (144-byte LDS
+// rows); TILE_MANY: 256 tokens, k-tiles of 32 (80-byte rows), which moves a
+// quarter fewer bytes into the CUs per FLOP but needs more workgroups to fill
+// the chip.  Both sum over k in the same order, so they give identical results.
+template <int SHAPE>
+struct Tile {
+    static constexpr int BT = SHAPE == TILE_MANY ? 4 : 2;     // 32-token blocks per wavefront
+    static constexpr int GTOK = 64 * BT;                       // tokens per workgroup
+    static constexpr int GK = SHAPE == TILE_MANY ? 32 : 64;    // k per LDS tile
+    static constexpr int GCH = GK / 8;                         // 16-byte chunks of data per row
+    static constexpr int GP = (GCH + 1) * 8;                   // row pitch in elements (one pad chunk)
+    static constexpr int ATILE = GF * GP;                      // W tile
+    static constexpr int STAGE = (GF + GTOK) * GP;             // W tile, then activation tile
+    static constexpr int OP = GF + 8;                          // output staging row pitch (elements)
+    static constexpr int ACH = GF * GCH / GT;                  // W chunks per thread and k-tile
+    static constexpr int BCH = GTOK * GCH / GT;                // activation chunks per thread and k-tile
+    static constexpr int SMEM = 2 * STAGE > GTOK * OP ? 2 * STAGE : GTOK * OP;
+    static_assert(GF * GCH % GT == 0 && GTOK * GCH % GT == 0, "chunks per thread");
+    static_assert((size_t)SMEM * sizeof(uint16_t) * 2 <= 160 * 1024, "two workgroups per CU must fit in LDS");
+};
 
 enum { ACT_ROWS = 0, ACT_HEADS = 1 };   // activations: [M][K] rows, or O [B][H][L][d]
 enum { OUT_QKV = 0, OUT_ROWS = 1 };     // epilogue: scatter to Q/K/V, or [M][N] rows
@@ -81,22 +98,24 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 }
 
 // Global -> register loads of k-tile kt: thread tid owns chunks
-// c = it * GT + tid of the W tile (it < 4) and of the activation tile
-// (it >= 4), chunk c being row c / 8, 16-byte column c % 8.  Token rows
-// beyond M load row M - 1 (their outputs are not stored).
-template <int ACT>
-__device__ __forceinline__ void load_gemm_tile(const GemmParams& p, int n0, int t0, int kt, int tid, u32x4 (&r)[8]) {
+// c = it * GT + tid of the W tile and of the activation tile, chunk c being
+// row c / GCH, 16-byte column c % GCH.  Token rows beyond M load row M - 1
+// (their outputs are not stored).
+template <int ACT, int SHAPE>
+__device__ __forceinline__ void load_gemm_tile(const GemmParams& p, int n0, int t0, int kt, int tid,
+                                               u32x4 (&r)[Tile<SHAPE>::ACH + Tile<SHAPE>::BCH]) {
+    using T = Tile<SHAPE>;
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < T::ACH; ++it) {
         const int c = it * GT + tid;
-        const int row = c >> 3, ch = c & 7;
-        r[it] = *(const u32x4*)(p.W + (size_t)(n0 + row) * p.K + kt * GK + ch * 8);
+        const int row = c / T::GCH, ch = c % T::GCH;
+        r[it] = *(const u32x4*)(p.W + (size_t)(n0 + row) * p.K + kt * T::GK + ch * 8);
     }
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < T::BCH; ++it) {
         const int c = it * GT + tid;
-        const int row = c >> 3, ch = c & 7;
-        const int kk = kt * GK + ch * 8;
+        const int row = c / T::GCH, ch = c % T::GCH;
+        const int kk = kt * T::GK + ch * 8;
         const int t = min(t0 + row, p.M - 1);
         const uint16_t* src;
         if constexpr (ACT == ACT_ROWS) {
@@ -106,27 +125,35 @@ __device__ __forceinline__ void load_gemm_tile(const GemmParams& p, int n0, int 
             const int h = kk / p.d, j = kk - h * p.d;
             src = p.act + ((size_t)(b * p.H + h) * p.L + l) * p.d + j;
         }
-        r[4 + it] = *(const u32x4*)src;
+        r[T::ACH + it] = *(const u32x4*)src;
     }
 }
 
-__device__ __forceinline__ void store_gemm_tile(int tid, const u32x4 (&r)[8], uint16_t* As, uint16_t* Bs) {
+template <int SHAPE>
+__device__ __forceinline__ void store_gemm_tile(int tid, const u32x4 (&r)[Tile<SHAPE>::ACH + Tile<SHAPE>::BCH],
+                                                uint16_t* As, uint16_t* Bs) {
+    using T = Tile<SHAPE>;
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
+    for (int it = 0; it < T::ACH; ++it) {
         const int c = it * GT + tid;
-        const int row = c >> 3, ch = c & 7;
-        *(u32x4*)(As + row * GP + ch * 8) = r[it];
-        *(u32x4*)(Bs + row * GP + ch * 8) = r[4 + it];
+        *(u32x4*)(As + (c / T::GCH) * T::GP + (c % T::GCH) * 8) = r[it];
+    }
+#pragma unroll
+    for (int it = 0; it < T::BCH; ++it) {
+        const int c = it * GT + tid;
+        *(u32x4*)(Bs + (c / T::GCH) * T::GP + (c % T::GCH) * 8) = r[T::ACH + it];
     }
 }
 
-template <int ACT, int OUT>
+template <int ACT, int OUT, int SHAPE>
 __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2))) gemm_kernel(GemmParams p) {
-    __shared__ __attribute__((aligned(16))) uint16_t smem[2 * G_STAGE];
+    using T = Tile<SHAPE>;
+    constexpr int BT = T::BT, GK = T::GK, GP = T::GP, GTOK = T::GTOK;
+    __shared__ __attribute__((aligned(16))) uint16_t smem[T::SMEM];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int wf = wave & 1, wt = wave >> 1;    // the wavefront's 64-feature and 64-token halves
+    const int wf = wave & 1, wt = wave >> 1;    // the wavefront's feature and token halves
     const int r32 = lane & 31, h = lane >> 5;
 
     int blk = blockIdx.x;
@@ -134,42 +161,42 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
     const int ft = blk % p.nft, tt = blk / p.nft;
     const int n0 = ft * GF, t0 = tt * GTOK;
 
-    f32x16 acc[2][2];
+    f32x16 acc[2][BT];
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
+        for (int nb = 0; nb < BT; ++nb)
 #pragma unroll
             for (int i = 0; i < 16; ++i) acc[mb][nb][i] = 0.f;
 
     const int nk = p.K / GK;
     int stage = 0;
-    u32x4 stg[8];
-    load_gemm_tile<ACT>(p, n0, t0, 0, tid, stg);
-    store_gemm_tile(tid, stg, smem, smem + G_TILE);
+    u32x4 stg[T::ACH + T::BCH];
+    load_gemm_tile<ACT, SHAPE>(p, n0, t0, 0, tid, stg);
+    store_gemm_tile<SHAPE>(tid, stg, smem, smem + T::ATILE);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
-        const uint16_t* As = smem + stage * G_STAGE;
-        const uint16_t* Bs = As + G_TILE;
-        if (kt + 1 < nk) load_gemm_tile<ACT>(p, n0, t0, kt + 1, tid, stg);
+        const uint16_t* As = smem + stage * T::STAGE;
+        const uint16_t* Bs = As + T::ATILE;
+        if (kt + 1 < nk) load_gemm_tile<ACT, SHAPE>(p, n0, t0, kt + 1, tid, stg);
         const uint16_t* arow = As + (64 * wf + r32) * GP + 8 * h;
-        const uint16_t* brow = Bs + (64 * wt + r32) * GP + 8 * h;
+        const uint16_t* brow = Bs + (32 * BT * wt + r32) * GP + 8 * h;
 #pragma unroll
         for (int ks = 0; ks < GK / 16; ++ks) {
-            bf16x8 a[2], b[2];
+            bf16x8 a[2], b[BT];
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb) a[mb] = __builtin_bit_cast(bf16x8, *(const u32x4*)(arow + 32 * mb * GP + 16 * ks));
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) b[nb] = __builtin_bit_cast(bf16x8, *(const u32x4*)(brow + 32 * nb * GP + 16 * ks));
+            for (int nb = 0; nb < BT; ++nb) b[nb] = __builtin_bit_cast(bf16x8, *(const u32x4*)(brow + 32 * nb * GP + 16 * ks));
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                for (int nb = 0; nb < 2; ++nb)
+                for (int nb = 0; nb < BT; ++nb)
                     acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mb], b[nb], acc[mb][nb], 0, 0, 0);
         }
         if (kt + 1 < nk) {
-            uint16_t* An = smem + (stage ^ 1) * G_STAGE;
-            store_gemm_tile(tid, stg, An, An + G_TILE);
+            uint16_t* An = smem + (stage ^ 1) * T::STAGE;
+            store_gemm_tile<SHAPE>(tid, stg, An, An + T::ATILE);
         }
         __syncthreads();
         stage ^= 1;
@@ -180,8 +207,8 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
     // order (the loop ended on a barrier, so every stage is free)
     uint16_t* ot = smem;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        const int tl = 64 * wt + 32 * nb + r32;
+    for (int nb = 0; nb < BT; ++nb) {
+        const int tl = 32 * BT * wt + 32 * nb + r32;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb) {
 #pragma unroll
@@ -189,7 +216,7 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
                 const int fl = 64 * wf + 32 * mb + 8 * jb + 4 * h;
                 f32x4 v{acc[mb][nb][4 * jb], acc[mb][nb][4 * jb + 1], acc[mb][nb][4 * jb + 2], acc[mb][nb][4 * jb + 3]};
                 if (p.bias) v += *(const f32x4*)(p.bias + n0 + fl);
-                *(u32x2*)(ot + tl * G_OP + fl) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                *(u32x2*)(ot + tl * T::OP + fl) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
             }
         }
     }
@@ -201,7 +228,7 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
         const int tl = c / (GF / 8), g = c % (GF / 8);
         const int t = t0 + tl;
         if (t >= p.M) continue;
-        const u32x4 val = *(const u32x4*)(ot + tl * G_OP + 8 * g);
+        const u32x4 val = *(const u32x4*)(ot + tl * T::OP + 8 * g);
         const int f = n0 + 8 * g;
         if constexpr (OUT == OUT_QKV) {
             const int b = t / p.L, l = t - b * p.L;
@@ -214,16 +241,25 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
     }
 }
 
+template <int ACT, int OUT, int SHAPE>
+hipError_t launch_shape(GemmParams& p, hipStream_t stream) {
+    constexpr int GTOK = Tile<SHAPE>::GTOK;
+    const long long nb = (long long)((p.M + GTOK - 1) / GTOK) * p.nft;
+    if (nb <= 0 || nb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
+    p.nblocks = (int)nb;
+    hipLaunchKernelGGL((gemm_kernel<ACT, OUT, SHAPE>), dim3(p.nblocks), dim3(GT), 0, stream, p);
+    return hipGetLastError();
+}
+
+// The 256-token tile when it still gives every CU at least four rounds of two
+// workgroups (measured at 32768 tokens: the QKV projection gains about 10%
+// with it, the output projection, 2.25 rounds, loses about as much).
 template <int ACT, int OUT>
 hipError_t launch_gemm(GemmParams& p, hipStream_t stream) {
     p.nft = p.N / GF;
-    const long long ntt = (p.M + GTOK - 1) / GTOK;
-    const long long nb = ntt * p.nft;
-    if (nb <= 0 || nb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
-    p.nblocks = (int)nb;
-    static_assert((size_t)2 * G_STAGE * sizeof(uint16_t) * 2 <= 160 * 1024, "two workgroups per CU must fit in LDS");
-    hipLaunchKernelGGL((gemm_kernel<ACT, OUT>), dim3(p.nblocks), dim3(GT), 0, stream, p);
-    return hipGetLastError();
+    const long long many = (long long)((p.M + Tile<TILE_MANY>::GTOK - 1) / Tile<TILE_MANY>::GTOK) * p.nft;
+    if (many >= 4LL * 2 * 256) return launch_shape<ACT, OUT, TILE_MANY>(p, stream);
+    return launch_shape<ACT, OUT, TILE_FEW>(p, stream);
 }
 
 }  // namespace
