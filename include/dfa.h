@@ -33,13 +33,18 @@
  *            unconditional partner of entry b (Sec. 3.4).
  *   Sizes    B, H, L >= 1; w >= 0; d in {64, 72} (others return
  *            DFA_ERR_UNSUPPORTED).  L is arbitrary: ragged tiles are masked.
+ *            Limits (DFA_ERR_INVALID_ARG beyond them): L <= 2^30, B*H <= 2^24,
+ *            B*H*L*d <= 2^40 elements, and B*L <= 2^30 tokens for the
+ *            projection and module entry points.
  *   Streams  Every call is asynchronous on `stream` (0 = the null stream).
  *            Outputs are valid once the caller has synchronised the stream.
  *   Memory   The caller allocates and owns every buffer and the stream.  The
- *            library never allocates, frees or synchronises, keeps no pointer
- *            after returning and holds no state between calls: calls are
- *            re-entrant and calls on different streams may run concurrently
- *            as long as their output buffers do not overlap.
+ *            library never allocates or frees and keeps no pointer after
+ *            returning; only dfa_plan_search synchronises (its stream, to read
+ *            each trial's loss).  The one state kept between calls is the
+ *            thread-local message of dfa_last_error().  Calls are re-entrant,
+ *            and calls on different streams may run concurrently as long as
+ *            their output buffers do not overlap.
  *   Errors   Every function returns a dfa_status; nothing else crosses the
  *            ABI.  Arguments are validated before any HIP call is made, so a
  *            bad argument is reported without touching a device.  After a

@@ -54,6 +54,8 @@ dfa_status check_shape(int B, int H, int L, int d, int w, Shape* s) {
     if (B <= 0 || H <= 0 || L <= 0 || d <= 0)
         return fail(DFA_ERR_INVALID_ARG, "sizes must be positive (B=%d H=%d L=%d d=%d)", B, H, L, d);
     if (w < 0) return fail(DFA_ERR_INVALID_ARG, "window half-width w=%d must be >= 0", w);
+    // token indexes (plus a tile) are int arithmetic in the kernels
+    if (L > (1 << 30)) return fail(DFA_ERR_INVALID_ARG, "L=%d is too large (at most 2^30 tokens)", L);
     const unsigned long long elems = (unsigned long long)B * H * L * d;
     if (elems > (1ULL << 40)) return fail(DFA_ERR_INVALID_ARG, "tensor of %llu elements is too large", elems);
     if ((unsigned long long)B * H > (1ULL << 24)) return fail(DFA_ERR_INVALID_ARG, "B*H=%lld is too large", (long long)B * H);
@@ -281,6 +283,9 @@ dfa_status check_regions(const Region* outs, int nout, const Region* ins, int ni
 dfa_status check_proj_shape(int B, int H, int L, int d, Shape* s) {
     dfa_status st;
     if ((st = check_shape(B, H, L, d, 0, s)) != DFA_OK) return st;
+    // the projections index the B * L tokens with int arithmetic
+    if ((long long)B * L > (1LL << 30))
+        return fail(DFA_ERR_INVALID_ARG, "B*L=%lld tokens is too large for a projection (at most 2^30)", (long long)B * L);
     if (!dfa::proj_shape_supported(H, d))
         return fail(DFA_ERR_UNSUPPORTED, "projection width H*d=%d is not a multiple of 128 (H=%d d=%d)", H * d, H, d);
     return DFA_OK;

@@ -137,6 +137,20 @@ def test_plan_null_arrays(L):
     assert L.dfa_plan_make(ctypes.c_uint64(1), 2, 2, 0, 2, None, None, None) == dfa.DFA_ERR_INVALID_ARG
 
 
+def test_size_limits(L):
+    """Token counts that the kernels' int index arithmetic cannot hold are
+    rejected before any launch (the tensors themselves would fit in HBM)."""
+    f = L.dfa_attn_full
+    assert f(A, B_, C_, D_, None, 1, 1, (1 << 30) + 1, 64, 8, None) == dfa.DFA_ERR_INVALID_ARG
+    assert "too large" in dfa.last_error()
+    big = 0x1000000
+    X, W, Q, K, V = (big * (i + 1) for i in range(5))
+    # B * L = 2^31 tokens at C = 128: 2^38 elements, within the tensor limit
+    assert L.dfa_qkv_proj(X, W, None, Q, K, V, 2, 2, 1 << 30, 64, None) == dfa.DFA_ERR_INVALID_ARG
+    assert "B*L" in dfa.last_error()
+    assert L.dfa_out_proj(Q, W, None, X, 2, 2, 1 << 30, 64, None) == dfa.DFA_ERR_INVALID_ARG
+
+
 def test_projection_validation(L):
     fq, fo, fm = L.dfa_qkv_proj, L.dfa_out_proj, L.dfa_module_step
     big = 0x1000000
