@@ -130,6 +130,36 @@ def test_kernels_vs_oracle(B, H, L, d, w):
         assert torch.equal(O4, O1.t), "a band covering every key must reproduce full attention bitwise"
 
 
+def test_long_sequence_sampled():
+    """L = 65536 (four times the 2K workload's tokens) through the three
+    kernels, on sampled query rows: the first and last rows, the rows at the
+    band edges next to the sequence ends and at key-tile boundaries, and a
+    seeded sample."""
+    dev = torch.device("cuda")
+    B, H, L, d, w = 1, 2, 65536, 72, 8192
+    shape = (B, H, L, d)
+    q, k, v = rand_qkv(shape, 65536)
+    Rres = rand_qkv(shape, 65537)[0].float() * 0.1
+    gq, gk, gv, gr = (t.to(dev) for t in (q, k, v, Rres))
+    O1, O2, O3 = (torch.empty(shape, dtype=torch.bfloat16, device=dev) for _ in range(3))
+    R2 = torch.empty(shape, dtype=torch.float32, device=dev)
+    say(f"long sequence B={B} H={H} L={L} d={d} w={w}")
+    dfa.dfa_attn_full(gq, gk, gv, O1, w)
+    dfa.dfa_attn_full_and_residual(gq, gk, gv, O2, R2, w)
+    dfa.dfa_attn_window_plus_residual(gq, gk, gv, O3, gr, w)
+    torch.cuda.synchronize()
+    fixed = [0, 1, 63, 64, 127, 128, w - 1, w, w + 1, L // 2, L - w - 2, L - w - 1, L - 129, L - 128,
+             L - 65, L - 64, L - 2, L - 1]
+    rows = np.unique(np.concatenate([fixed, np.random.default_rng(65536).integers(0, L, 48)]))
+    Qd, Kd, Vd = f64(q), f64(k), f64(v)
+    Of = orc.attention_rows(Qd, Kd, Vd, rows, None)
+    Wd = orc.attention_rows(Qd, Kd, Vd, rows, w)
+    check("long full", O1, Of, rows)
+    check("long refresh O", O2, Of, rows)
+    check("long refresh R", R2, Of - Wd, rows)
+    check("long window + R", O3, Wd + f64(Rres)[:, :, rows], rows)
+
+
 def test_window_without_residual_and_determinism():
     dev = torch.device("cuda")
     shape = (2, 3, 700, 72)
