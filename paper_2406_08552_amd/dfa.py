@@ -215,16 +215,25 @@ def dfa_module_step(code: int, X, Wqkv, bqkv, Wo, bo, Q, K, V, O, R, Y, Ycache, 
                                  _ptr(V), _ptr(O), _ptr(R), _ptr(Y), _ptr(Ycache), B, H, L, d, w, _stream(stream)))
 
 
+def _on_gpu(*named):
+    for t, name in named:
+        if t.device.type != "cuda" or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous GPU tensor (got {t.device})")
+
+
+def _nbytes(t) -> int:
+    return t.numel() * t.element_size()
+
+
 def dfa_mrae(A, B, workspace, result, stream=None) -> None:
     """result (a 1-element fp64 GPU tensor) = MRAE of two bf16 tensors of the
-    same size; workspace: a uint8 GPU tensor of MRAE_WORKSPACE_BYTES."""
+    same size; workspace: a GPU tensor of at least MRAE_WORKSPACE_BYTES bytes."""
     import torch
     if A.dtype != torch.bfloat16 or B.dtype != torch.bfloat16 or A.numel() != B.numel():
         raise ValueError("A and B must be bf16 tensors of the same size")
-    if not (A.is_contiguous() and B.is_contiguous()):
-        raise ValueError("A and B must be contiguous")
-    if workspace.numel() < MRAE_WORKSPACE_BYTES or result.dtype != torch.float64:
-        raise ValueError("workspace too small or result not fp64")
+    _on_gpu((A, "A"), (B, "B"), (workspace, "workspace"), (result, "result"))
+    if _nbytes(workspace) < MRAE_WORKSPACE_BYTES or result.dtype != torch.float64 or result.numel() < 1:
+        raise ValueError("workspace too small or result not an fp64 tensor")
     _check(lib().dfa_mrae(_ptr(A), _ptr(B), A.numel(), _ptr(workspace), _ptr(result), _stream(stream)))
 
 
@@ -235,24 +244,33 @@ def plan_search_workspace_bytes(n_layers: int, B: int, H: int, L: int, d: int) -
 def dfa_plan_search(X_steps, layers, delta: float, w: int, H: int, workspace, stream=None):
     """Greedy plan search (see include/dfa.h) over hidden states X_steps (list of
     [B, L, C] bf16 GPU tensors) and layers (list of (Wqkv, bqkv, Wo, bo) GPU
-    tensors); workspace: a uint8 GPU tensor of plan_search_workspace_bytes().
+    tensors); workspace: a GPU tensor of at least plan_search_workspace_bytes()
+    bytes.  Biases are given for every layer or for none.
     Returns (plan int32 [T, n_layers], loss float64 [T, n_layers])."""
     import torch
+    if not X_steps or not layers:
+        raise ValueError("X_steps and layers must be non-empty")
     B, L, C = X_steps[0].shape
+    if H <= 0 or C % H:
+        raise ValueError(f"C={C} is not a multiple of H={H}")
     d = C // H
     for X in X_steps:
         _expect(X, torch.bfloat16, (B, L, C), "X_steps[t]")
     for Wqkv, bqkv, Wo, bo in layers:
         _weights(Wqkv, bqkv, Wo, bo, C)
+    _on_gpu((workspace, "workspace"))
     T, n = len(X_steps), len(layers)
     arr = lambda ts: (ctypes.c_void_p * len(ts))(*[_ptr(t) for t in ts])  # noqa: E731
-    has_b = all(l[1] is not None for l in layers) and all(l[3] is not None for l in layers)
+    biased = [(l[1] is not None, l[3] is not None) for l in layers]
+    has_b = all(a and b for a, b in biased)
+    if not has_b and any(a or b for a, b in biased):
+        raise ValueError("give both biases for every layer or for none")
     plan = np.full((T, n), -1, dtype=np.int32)
     loss = np.full((T, n), np.nan)
     _check(lib().dfa_plan_search(n, T, arr(X_steps), arr([l[0] for l in layers]),
                                  arr([l[1] for l in layers]) if has_b else None, arr([l[2] for l in layers]),
                                  arr([l[3] for l in layers]) if has_b else None, float(delta), B, H, L, d, w,
-                                 _ptr(workspace), workspace.numel(), plan.ctypes.data_as(_i32p),
+                                 _ptr(workspace), _nbytes(workspace), plan.ctypes.data_as(_i32p),
                                  loss.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), _stream(stream)))
     return plan, loss
 

@@ -203,3 +203,19 @@ def test_search_and_mrae_validation(L):
     assert "too small" in dfa.last_error()
     assert f(*args, 0.1, 2, 2, 64, 64, 8, 0x400010, need, pp, lp, None) == dfa.DFA_ERR_INVALID_ARG
     assert f(*args, 0.1, 2, 2, 64, 64, 8, 0x400000, need, None, lp, None) == dfa.DFA_ERR_INVALID_ARG
+
+
+def test_binding_rejects_host_tensors():
+    """The binding refuses host tensors before any device pointer reaches the
+    library (a host address written by a kernel would fault the GPU)."""
+    import torch
+    a = torch.zeros(64, dtype=torch.bfloat16)
+    ws = torch.zeros(dfa.MRAE_WORKSPACE_BYTES, dtype=torch.uint8)
+    res = torch.zeros(1, dtype=torch.float64)
+    with pytest.raises(ValueError, match="GPU"):
+        dfa.dfa_mrae(a, a, ws, res)
+    with pytest.raises(ValueError, match="non-empty"):
+        dfa.dfa_plan_search([], [], 0.1, 4, 2, ws)
+    q = torch.zeros((1, 1, 64, 64), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU"):
+        dfa.dfa_attn_full(q, q, q, q.clone(), 0)
