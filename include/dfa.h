@@ -236,6 +236,8 @@ dfa_status dfa_plan_search(int n_layers, int n_steps, const void* const* X_steps
  *      refresh_every steps old, else REUSE
  *   3. refresh_every == 0: REUSE before the layer's first refresh -> REFRESH
  *   4. ASC drawn with an odd B                             -> DFA_ERR_INVALID_ARG
+ *      (the entries before it are already written; the arrays' contents are
+ *      then unspecified)
  * n_layers, n_steps, B >= 1 and refresh_every >= 0 are required. */
 dfa_status dfa_plan_make(uint64_t seed, int n_layers, int n_steps, int refresh_every, int B,
                          int32_t* code, int32_t* r_src, int32_t* o_src);

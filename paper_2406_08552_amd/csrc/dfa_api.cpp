@@ -19,13 +19,17 @@ namespace {
 
 thread_local std::string g_last_error;
 
-dfa_status fail(dfa_status st, const char* fmt, ...) {
+void vrecord(const char* fmt, va_list ap) {
     char buf[512];
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    g_last_error = buf;
+}
+
+dfa_status fail(dfa_status st, const char* fmt, ...) {
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
+    vrecord(fmt, ap);
     va_end(ap);
-    g_last_error = buf;
     return st;
 }
 
@@ -127,12 +131,10 @@ dfa_status check_cache(const void* O, const void* Oc, const void* Q, const void*
 }  // namespace
 
 int dfa::set_error(int status, const char* fmt, ...) {
-    char buf[512];
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
+    vrecord(fmt, ap);
     va_end(ap);
-    g_last_error = buf;
     return status;
 }
 
