@@ -160,6 +160,50 @@ def test_long_sequence_sampled():
     check("long window + R", O3, Wd + f64(Rres)[:, :, rows], rows)
 
 
+def test_concurrent_streams_match_serial():
+    """Calls on two streams (default priority) with disjoint outputs run
+    concurrently and give the same bits as the same calls made one after the
+    other: the library keeps no state between calls."""
+    dev = torch.device("cuda")
+    shape_a, shape_b = (2, 4, 1024, 72), (1, 8, 777, 64)
+    qa, ka, va = (t.to(dev) for t in rand_qkv(shape_a, 91))
+    qb, kb, vb = (t.to(dev) for t in rand_qkv(shape_b, 92))
+    say("two streams: refresh + reuse on one, full + short-sequence on the other")
+    qs, ks, vs = (t.to(dev) for t in rand_qkv((8, 16, 16, 72), 93))
+
+    def work(outs):
+        Oa, Ra, Oa2, Ob, Os = outs
+        return [lambda: dfa.dfa_attn_full_and_residual(qa, ka, va, Oa, Ra, 128),
+                lambda: dfa.dfa_attn_window_plus_residual(qa, ka, va, Oa2, Ra, 128),
+                lambda: dfa.dfa_attn_full(qb, kb, vb, Ob, 0),
+                lambda: dfa.dfa_plan_step(dfa.WARS_REFRESH, qs, ks, vs, Os, torch.empty(qs.shape, dtype=torch.float32,
+                                                                                        device=dev), None, 2)]
+
+    def fresh():
+        return (torch.empty(shape_a, dtype=torch.bfloat16, device=dev), torch.empty(shape_a, dtype=torch.float32, device=dev),
+                torch.empty(shape_a, dtype=torch.bfloat16, device=dev), torch.empty(shape_b, dtype=torch.bfloat16, device=dev),
+                torch.empty(qs.shape, dtype=torch.bfloat16, device=dev))
+
+    serial = fresh()
+    for f in work(serial):
+        f()
+    torch.cuda.synchronize()
+    conc = fresh()
+    fa, fb = work(conc)[:2], work(conc)[2:]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            for f in fa:
+                f()
+        with torch.cuda.stream(s2):
+            for f in fb:
+                f()
+    torch.cuda.synchronize()
+    for a, b in zip(serial, conc):
+        assert torch.equal(a, b), "concurrent streams changed a result"
+
+
 def test_window_without_residual_and_determinism():
     dev = torch.device("cuda")
     shape = (2, 3, 700, 72)
