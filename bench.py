@@ -100,16 +100,20 @@ def video_bench(args, dfa, inputs, torch, dev, stream):
         R = torch.empty(shape, dtype=torch.float32, device=dev)
         full = 4.0 * B * H * L * L * d
         band = 4.0 * B * H * d * n_band(L, w)
+        # (entry, algorithmic FLOPs, algorithmic bytes in bf16 tensors: Q, K, V read and O
+        # written; the fp32 residual counts two; ASC reads half of Q, K, V)
         runs = {
-            "full": (lambda: dfa.dfa_attn_full(q, k, v, O, w, stream), full),
-            "wars_refresh": (lambda: dfa.dfa_attn_full_and_residual(q, k, v, O, R, w, stream), full),
-            "wars_reuse": (lambda: dfa.dfa_attn_window_plus_residual(q, k, v, O, R, w, stream), band),
-            "asc": (lambda: dfa.dfa_plan_step(dfa.ASC_REUSE, q, k, v, O, None, None, w, stream), full / 2),
+            "full": (lambda: dfa.dfa_attn_full(q, k, v, O, w, stream), full, 4),
+            "wars_refresh": (lambda: dfa.dfa_attn_full_and_residual(q, k, v, O, R, w, stream), full, 6),
+            "wars_reuse": (lambda: dfa.dfa_attn_window_plus_residual(q, k, v, O, R, w, stream), band, 6),
+            "asc": (lambda: dfa.dfa_plan_step(dfa.ASC_REUSE, q, k, v, O, None, None, w, stream), full / 2, 2.5),
         }
+        tensor_bytes = B * H * L * d * 2
         res = {"B": B, "L": L, "w": w}
-        for name, (fn, fl) in runs.items():
+        for name, (fn, fl, ntens) in runs.items():
             ms = timed(torch, stream, fn, args.kernel_reps)
-            res[name] = {"ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 1)}
+            res[name] = {"ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 1),
+                         "gbs": round(ntens * tensor_bytes / (ms * 1e-3) / 1e9, 1)}
         out[cfg.name] = res
     return out
 
