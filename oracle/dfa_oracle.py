@@ -13,7 +13,8 @@ the paper's order and notation (DiTFastAttn, arXiv 2406.08552):
                                  the diagonal of the attention matrix), Eq. (1)-(2)
   * WA-RS refresh             -- Sec. 3.2, Eq. (1):  R_r = O_r - W_r
   * WA-RS reuse               -- Sec. 3.2, Eq. (2):  O_k = W_k + R_r
-  * AST                       -- Sec. 3.3: reuse the cached earliest-step output
+  * AST                       -- Sec. 3.3: a step returns the output kept from the
+                                 first step of its run of similar steps
   * ASC                       -- Sec. 3.4: reuse the conditional half's output for
                                  the unconditional half
   * plan + cache bookkeeping  -- Sec. 3.5 / Alg. 1 output dictionary (per layer,
@@ -23,9 +24,12 @@ the paper's order and notation (DiTFastAttn, arXiv 2406.08552):
                                  module, window = 1/8 of the tokens, Sec. 4.1)
   * the attention module      -- QKV projection, attention under the plan, output
                                  projection; AST/ASC skip or halve the whole module
+  * MRAE and the plan search  -- Sec. 3.5, Alg. 1: the loss between the compressed and
+                                 the uncompressed model's outputs, and the greedy
+                                 per-step, per-layer choice of strategy, run on a
+                                 surrogate model of attention modules
 
-Readings of points the paper leaves open (all listed with reasons in the
-design notes):
+Readings of points the paper leaves open:
   - the window is a 1D band over the flattened token index, |i - j| <= w,
     symmetric and non-causal, truncated at 0 and L-1; w is the half-width;
   - the softmax scale is 1/sqrt(d);
