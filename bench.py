@@ -262,7 +262,7 @@ def cpu_baseline(cfg, target_s: float):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1"}), flush=True)
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; --gpus must be 1"}), flush=True)
         sys.exit(2)
 
     import torch
