@@ -371,8 +371,11 @@ def main():
         s1.record(stream)
         torch.cuda.synchronize()
         ms = s0.elapsed_time(s1) / args.kernel_reps
-        kres[name] = {"ms": round(ms, 4), "tflops": round(fl / (ms * 1e-3) / 1e12, 1) if fl else 0.0,
-                      "gbs": round(ntens * tensor_bytes / (ms * 1e-3) / 1e9, 1)}
+        tflops = fl / (ms * 1e-3) / 1e12 if fl else 0.0
+        gbs = ntens * tensor_bytes / (ms * 1e-3) / 1e9
+        kres[name] = {"ms": round(ms, 4), "tflops": round(tflops, 1), "gbs": round(gbs, 1),
+                      "frac_of_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+                      "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4)}
 
     module = module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres)
     video = video_bench(args, dfa, inputs, torch, dev, stream)
