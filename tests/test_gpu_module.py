@@ -76,6 +76,35 @@ def test_projections_vs_oracle(B, H, L, d):
     check("out_proj Y (no bias)", Y.t, orc.out_proj(f64(Ot), ow.Wo, None))
 
 
+def test_projections_large_sampled():
+    """58200 tokens: enough for the 256-token GEMM tiles in both projections
+    (at least four rounds of two workgroups per CU), with a ragged last token
+    tile of 88; checked on sampled tokens (the projections act per token)."""
+    dev = torch.device("cuda")
+    B, H, L, d = 1, 16, 58200, 72
+    C = H * d
+    (Wqkv, bqkv, Wo, bo), ow = _weights(H, d, 77, dev)
+    X = inputs.DriftingX(11, 0, (B, L, C)).advance()
+    shape = (B, H, L, d)
+    Q, K, V = (Guarded(shape, dev) for _ in range(3))
+    say(f"qkv_proj B={B} H={H} L={L} d={d} (256-token tiles)")
+    dfa.dfa_qkv_proj(X.to(dev), Wqkv, bqkv, Q.t, K.t, V.t)
+    torch.cuda.synchronize()
+    fixed = [0, 1, 127, 128, 255, 256, L - 89, L - 88, L - 87, L - 2, L - 1]
+    rows = np.unique(np.concatenate([fixed, np.random.default_rng(L).integers(0, L, 96)]))
+    refs = orc.qkv_proj(f64(X)[:, rows], ow.Wqkv, ow.bqkv, H)
+    for name, got, ref in zip("QKV", (Q, K, V), refs):
+        check(f"qkv_proj {name}", got.t, ref, rows)
+        assert got.guards_intact(), f"write outside {name}"
+    Ot = torch.randn(shape, generator=torch.Generator().manual_seed(L)).to(torch.bfloat16)
+    Y = Guarded((B, L, C), dev)
+    say(f"out_proj B={B} H={H} L={L} d={d} (256-token tiles)")
+    dfa.dfa_out_proj(Ot.to(dev), Wo, bo, Y.t)
+    torch.cuda.synchronize()
+    check("out_proj Y", Y.t[:, rows], orc.out_proj(f64(Ot)[:, :, rows], ow.Wo, ow.bo))
+    assert Y.guards_intact(), "write outside Y"
+
+
 @pytest.mark.parametrize("B,H,L,d,w,alias", [(2, 16, 256, 72, 32, False), (4, 16, 200, 72, 24, True),
                                              (2, 2, 97, 64, 0, False)])
 def test_module_plan_vs_oracle(B, H, L, d, w, alias):
