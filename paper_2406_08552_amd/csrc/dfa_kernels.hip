@@ -11,7 +11,10 @@
 //   (batch, head); each wavefront owns 32 of them (two 16-query MFMA blocks).
 //   The workgroup walks key tiles of BK = 64 keys, staged in LDS with double
 //   buffering (global loads of the next tile are in flight while the current
-//   one is used).  Three workgroups share a CU (three wavefronts per SIMD), so
+//   one is used).  A whole tile is copied from a uniform tile base plus
+//   per-lane offsets that do not depend on the tile, so the copies take the
+//   scalar-base addressing form and cost the softmax no VALU work; only the
+//   ragged last tile clamps its rows.  Three workgroups share a CU (three wavefronts per SIMD), so
 //   the MFMA work of one overlaps the softmax arithmetic of the others.
 //
 // MFMA mapping (v_mfma_f32_16x16x32_bf16, fp32 accumulation)
@@ -357,7 +360,34 @@ template <int D>
 __device__ __forceinline__ void issue_tile(const uint16_t* __restrict__ Kbh, const uint16_t* __restrict__ Vbh, int k0,
                                            int L, int tid, uint16_t* Ks, uint16_t* Vs) {
     using G = Geo<D>;
-    const int wave_chunk0 = tid & ~63;   // first chunk of this wavefront in a round
+    // first chunk of this wavefront in a round: uniform, kept in a scalar
+    // register so the LDS destination (M0) needs no per-copy lane read
+    const int wave_chunk0 = __builtin_amdgcn_readfirstlane(tid & ~63);
+    if (k0 + BK <= L) {
+        // whole tile: a uniform tile base plus a per-lane offset that does not
+        // depend on the tile (loop-invariant, so no address arithmetic per copy)
+        const uint16_t* kb = Kbh + (size_t)k0 * D;
+        const uint16_t* vb = Vbh + (size_t)k0 * D;
+#pragma unroll
+        for (int it = 0; it < G::KROUNDS; ++it) {
+            const int c = it * NTHREADS + tid;
+            const int row = c / G::KPC, ch = c % G::KPC;
+            if (row < BK && ch < G::NCH)
+                __builtin_amdgcn_global_load_lds((const void*)(kb + (uint32_t)(row * D + ch * 8)),
+                                                 (__attribute__((address_space(3))) void*)(Ks + (it * NTHREADS + wave_chunk0) * 8),
+                                                 16, 0, 0);
+        }
+#pragma unroll
+        for (int it = 0; it < G::VROUNDS; ++it) {
+            const int c = it * NTHREADS + tid;
+            const int row = c / G::VPC, ch = c % G::VPC;
+            if (row < BK && ch < G::NCH)
+                __builtin_amdgcn_global_load_lds((const void*)(vb + (uint32_t)(row * D + ch * 8)),
+                                                 (__attribute__((address_space(3))) void*)(Vs + (it * NTHREADS + wave_chunk0) * 8),
+                                                 16, 0, 0);
+        }
+        return;
+    }
 #pragma unroll
     for (int it = 0; it < G::KROUNDS; ++it) {
         const int c = it * NTHREADS + tid;
