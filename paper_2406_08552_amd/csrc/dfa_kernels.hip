@@ -32,6 +32,8 @@
 //   PV pads the 72 output dims to 5 blocks of 16.  The
 //   padding row 72 of V^T is set to 1.0, so the PV product also yields the
 //   softmax row sum (the sum of the same bf16 probabilities that weight V).
+//   Head dim 64 has no padding row: the lanes sum the rounded probabilities
+//   themselves, so both head dims normalise exactly the weights they apply.
 //
 // Online softmax
 //   Per query a running max m (log2 domain) and accumulator (O, l).  The max
@@ -141,6 +143,14 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, bf16x2{(__bf16)lo, (__bf16)hi});
 }
 
+// acc + the two bf16 values packed in w (one dot2 with (1, 1)): the row sum
+// is taken over the same rounded probabilities that weight V, so each output
+// row is a convex combination of V rows (exact for a one-hot row).
+__device__ __forceinline__ float pair_acc(uint32_t w, float acc) {
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, acc, false);
+}
+
 // s_waitcnt vmcnt(0): every global access of this wavefront has completed.
 // The tile stores sit in branches that whole wavefronts skip; without this
 // the compiler cannot prove at the loop head that the Q fragments have
@@ -191,7 +201,7 @@ struct Acc {
     // The running max m (log2 domain) is kept in two derived forms:
     float negm[QBW];             // -m, or 0 while the query has seen no finite score
     float thr[QBW];              // (m + RESCALE_THRESH) / c in raw score units (-inf: no m yet)
-    float l[QBW];                // lane-partial row sum (unused when a ones row is present)
+    float l[QBW];                // lane-partial sum of the bf16 probabilities (unused when a ones row is present)
 
     __device__ __forceinline__ void init() {
 #pragma unroll
@@ -312,9 +322,9 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
                 const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[1], c, negm));
                 const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2], c, negm));
                 const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[3], c, negm));
-                if constexpr (!G::ONES) psum += (p0 + p1) + (p2 + p3);
                 wds[2 * half + 0] = pack_bf16x2(p0, p1);
                 wds[2 * half + 1] = pack_bf16x2(p2, p3);
+                if constexpr (!G::ONES) psum = pair_acc(wds[2 * half + 1], pair_acc(wds[2 * half], psum));
             }
             pb[qb][h] = as_bf16x8(u32x4{wds[0], wds[1], wds[2], wds[3]});
         }

@@ -77,11 +77,20 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, bf16x2{(__bf16)lo, (__bf16)hi});
 }
 
+// acc + the two bf16 values packed in w (one dot2 with (1, 1)): the row sum
+// is taken over the same rounded probabilities that weight V, so each output
+// row is a convex combination of V rows (exact for a one-hot row).
+__device__ __forceinline__ float pair_acc(uint32_t w, float acc) {
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, acc, false);
+}
+
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) { return *(const u32x4*)p; }
 
 // Probabilities of one query block (lane: query 16 qb + r, keys 16 kb + 4 g + i)
 // under the key set of BAND (all keys < L, or also |i - j| <= w), packed as
-// the PV B operand; psum gets the fp32 sum over the lane's keys.
+// the PV B operand; psum gets the fp32 sum of the packed (rounded) values
+// over the lane's keys.
 template <int NB, bool BAND>
 __device__ __forceinline__ bf16x8 probs(const f32x4 (&s)[NB], int qi, int g, int L, int w, float c, float& psum) {
     float v[NB][4];
@@ -107,9 +116,9 @@ __device__ __forceinline__ bf16x8 probs(const f32x4 (&s)[NB], int qi, int g, int
         float p[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(v[kb][i], c, negm));
-        psum += (p[0] + p[1]) + (p[2] + p[3]);
         wd[2 * kb + 0] = pack_bf16x2(p[0], p[1]);
         wd[2 * kb + 1] = pack_bf16x2(p[2], p[3]);
+        psum = pair_acc(wd[2 * kb + 1], pair_acc(wd[2 * kb], psum));
     }
     return __builtin_bit_cast(bf16x8, u32x4{wd[0], wd[1], wd[2], wd[3]});
 }

@@ -204,6 +204,44 @@ def test_concurrent_streams_match_serial():
         assert torch.equal(a, b), "concurrent streams changed a result"
 
 
+@pytest.mark.parametrize("kind,L,d,w", [("large", 2048, 72, 300), ("growing", 2048, 72, 300),
+                                         ("growing", 1000, 64, 77), ("large", 777, 64, 0)])
+def test_rescale_paths(kind, L, d, w):
+    """Inputs that drive the online softmax's rescale: scores of large spread
+    (Q and K scaled by 6, nearly one-hot rows), or scores that grow along the
+    keys so that most tiles raise the running maximum by more than the rescale
+    margin."""
+    dev = torch.device("cuda")
+    B, H = 1, 2
+    shape = (B, H, L, d)
+    g = torch.Generator().manual_seed(4242 + L + d)
+    q, k, v = (torch.randn(shape, generator=g) for _ in range(3))
+    if kind == "large":
+        q, k = 6 * q, 6 * k
+    else:
+        u = torch.randn(d, generator=g).sign()
+        ramp = torch.linspace(0, 20, L).view(1, 1, L, 1)
+        q = q + 2 * u
+        k = k + ramp * u
+    q, k, v = (t.to(torch.bfloat16) for t in (q, k, v))
+    Rres = rand_qkv(shape, 7 + L)[0].float() * 0.1
+    gq, gk, gv, gr = (t.to(dev) for t in (q, k, v, Rres))
+    O1, O2, O3 = (torch.empty(shape, dtype=torch.bfloat16, device=dev) for _ in range(3))
+    R2 = torch.empty(shape, dtype=torch.float32, device=dev)
+    say(f"rescale paths {kind} L={L} d={d} w={w}")
+    dfa.dfa_attn_full(gq, gk, gv, O1, w)
+    dfa.dfa_attn_full_and_residual(gq, gk, gv, O2, R2, w)
+    dfa.dfa_attn_window_plus_residual(gq, gk, gv, O3, gr, w)
+    torch.cuda.synchronize()
+    Qd, Kd, Vd = f64(q), f64(k), f64(v)
+    Of = orc.attn_full(Qd, Kd, Vd)
+    Wd = orc.attn_window(Qd, Kd, Vd, w)
+    check(f"{kind} full", O1, Of)
+    check(f"{kind} refresh O", O2, Of)
+    check(f"{kind} refresh R", R2, Of - Wd)
+    check(f"{kind} window + R", O3, Wd + f64(Rres))
+
+
 def test_window_without_residual_and_determinism():
     dev = torch.device("cuda")
     shape = (2, 3, 700, 72)
