@@ -256,18 +256,38 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
                                            int qrow0, int k0, int L, int w, float c) {
     using G = Geo<D>;
     if constexpr (MASK != MASK_NONE) {
+        // The lane's scores are the keys jbase + o, o = 16 kb + i.  Valid keys
+        // (j < L) are the offsets o <= lim.  For the in-band mask the band
+        // |qi - j| <= w, cut to [0, L - 1], is the offset range [a, b], tested
+        // as one unsigned compare (o - a <= b - a); a query row beyond L whose
+        // band holds no key gets an empty range.  The out-of-band mask keeps
+        // the direct distance test: the range form's two extra live values per
+        // query block cost the refresh kernel spills and time.
+        const int jbase = k0 + 4 * g;
+        const int lim = L - 1 - jbase;
 #pragma unroll
         for (int qb = 0; qb < QBW; ++qb) {
-            const int qi = qrow0 + 16 * qb + r;
+            int lo = 0;
+            uint32_t span = 0u;
+            if constexpr (MASK == MASK_BAND_IN) {
+                const int qi = qrow0 + 16 * qb + r;
+                const int a = (qi > w ? qi - w : 0) - jbase;
+                const uint32_t qpw = (uint32_t)qi + (uint32_t)w;    // < 2^32: qi < 2^31, w < 2^31
+                const int b = (int)(qpw < (uint32_t)(L - 1) ? qpw : (uint32_t)(L - 1)) - jbase;
+                lo = b < a ? (1 << 30) : a;
+                span = b < a ? 0u : (uint32_t)(b - a);
+            }
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int j = k0 + 16 * kb + 4 * g + i;
-                    bool ok = j < L;
-                    if constexpr (MASK == MASK_BAND_IN || MASK == MASK_BAND_OUT) {
-                        const int dist = qi > j ? qi - j : j - qi;
-                        ok = ok && ((MASK == MASK_BAND_IN) ? (dist <= w) : (dist > w));
+                    const int o = 16 * kb + i;
+                    bool ok;
+                    if constexpr (MASK == MASK_KEYS) ok = o <= lim;
+                    else if constexpr (MASK == MASK_BAND_IN) ok = (uint32_t)(o - lo) <= span;
+                    else {
+                        const int j = jbase + o, qi = qrow0 + 16 * qb + r;
+                        ok = j < L && (qi > j ? qi - j : j - qi) > w;
                     }
                     S.s[qb][kb][i] = ok ? S.s[qb][kb][i] : NEG_INF;
                 }

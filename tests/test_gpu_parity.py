@@ -242,6 +242,32 @@ def test_rescale_paths(kind, L, d, w):
     check(f"{kind} window + R", O3, Wd + f64(Rres))
 
 
+@pytest.mark.parametrize("B,H,L,d", [(1, 2, 333, 72), (1, 2, 200, 64), (3, 2, 16, 72)])
+def test_extreme_half_widths(B, H, L, d):
+    """Half-widths at and far beyond the sequence (up to the largest int):
+    a band that covers every key gives the window attention of full attention
+    and a residual of exactly zero; one key short of that it is a true band."""
+    dev = torch.device("cuda")
+    shape = (B, H, L, d)
+    q, k, v = rand_qkv(shape, 900 + L + d)
+    gq, gk, gv = (t.to(dev) for t in (q, k, v))
+    Qd, Kd, Vd = f64(q), f64(k), f64(v)
+    Of = orc.attn_full(Qd, Kd, Vd)
+    for w in [L - 2, L - 1, L, 1 << 30, (1 << 31) - 1]:
+        say(f"extreme half-width B={B} H={H} L={L} d={d} w={w}")
+        O1, O2 = (torch.empty(shape, dtype=torch.bfloat16, device=dev) for _ in range(2))
+        R = torch.full(shape, 7.0, dtype=torch.float32, device=dev)
+        dfa.dfa_attn_window_plus_residual(gq, gk, gv, O1, None, w)
+        dfa.dfa_attn_full_and_residual(gq, gk, gv, O2, R, w)
+        torch.cuda.synchronize()
+        check(f"window w={w}", O1, orc.attn_window(Qd, Kd, Vd, w))
+        check(f"refresh O w={w}", O2, Of)
+        if w >= L - 1:
+            assert torch.count_nonzero(R).item() == 0, f"w={w}: R must be exactly zero"
+        else:
+            check(f"refresh R w={w}", R, Of - orc.attn_window(Qd, Kd, Vd, w))
+
+
 def test_window_without_residual_and_determinism():
     dev = torch.device("cuda")
     shape = (2, 3, 700, 72)
