@@ -7,8 +7,10 @@
 // The window is the band |i - j| <= w over the flattened token index.
 //
 // Work decomposition
-//   A workgroup is 4 wavefronts and owns BQ = 128 consecutive queries of one
-//   (batch, head); each wavefront owns 32 of them (two 16-query MFMA blocks).
+//   A workgroup is 4 wavefronts and owns 128 consecutive queries of one
+//   (batch, head); each wavefront owns 32 of them (two 16-query MFMA blocks,
+//   QB = 2).  Launches whose tile walk is short (small L or a narrow band)
+//   use QB = 1 instead: 64-query workgroups, four wavefronts per SIMD.
 //   The workgroup walks key tiles of BK = 64 keys, staged in LDS with double
 //   buffering (global loads of the next tile are in flight while the current
 //   one is used).  A whole tile is copied from a uniform tile base plus
@@ -77,8 +79,9 @@ constexpr int NWAVES = 4;
 constexpr int NTHREADS = NWAVES * 64;
 constexpr int BK = 64;                    // keys per tile
 constexpr int NKB = BK / 16;              // 16-key blocks per tile
-constexpr int QBW = 2;                    // 16-query blocks per wavefront
-constexpr int BQ = NWAVES * QBW * 16;     // queries per workgroup
+// A wavefront owns QB 16-query blocks (QB = 1 or 2), a workgroup bq<QB>() queries.
+template <int QB>
+constexpr int bq() { return NWAVES * QB * 16; }
 constexpr float RESCALE_THRESH = 8.0f;    // lazy rescale margin (log2 units)
 constexpr float NEG_INF = -__builtin_inff();
 
@@ -191,21 +194,22 @@ __device__ __forceinline__ float group_sum(float x) {
 }
 
 // One score tile, passed by value where a masked private copy is needed.
+template <int QB>
 struct Tile {
-    f32x4 s[QBW][NKB];
+    f32x4 s[QB][NKB];
 };
 
-template <int D>
+template <int D, int QB>
 struct Acc {
-    f32x4 o[QBW][Geo<D>::NDB];   // O^T: lane holds dims 16*m + 4*g + i of query lane%16
+    f32x4 o[QB][Geo<D>::NDB];   // O^T: lane holds dims 16*m + 4*g + i of query lane%16
     // The running max m (log2 domain) is kept in two derived forms:
-    float negm[QBW];             // -m, or 0 while the query has seen no finite score
-    float thr[QBW];              // (m + RESCALE_THRESH) / c in raw score units (-inf: no m yet)
-    float l[QBW];                // lane-partial sum of the bf16 probabilities (unused when a ones row is present)
+    float negm[QB];             // -m, or 0 while the query has seen no finite score
+    float thr[QB];              // (m + RESCALE_THRESH) / c in raw score units (-inf: no m yet)
+    float l[QB];                // lane-partial sum of the bf16 probabilities (unused when a ones row is present)
 
     __device__ __forceinline__ void init() {
 #pragma unroll
-        for (int qb = 0; qb < QBW; ++qb) {
+        for (int qb = 0; qb < QB; ++qb) {
 #pragma unroll
             for (int mb = 0; mb < Geo<D>::NDB; ++mb) o[qb][mb] = f32x4{0.f, 0.f, 0.f, 0.f};
             negm[qb] = 0.f;
@@ -215,17 +219,17 @@ struct Acc {
     }
 };
 
-template <int D>
+template <int D, int QB>
 struct QFrag {
-    bf16x8 a[QBW][Geo<D>::NC32 > 0 ? Geo<D>::NC32 : 1];
-    bf16x8 t[QBW];   // dims D32.. in lane rows g < TAIL/8, zero elsewhere
+    bf16x8 a[QB][Geo<D>::NC32 > 0 ? Geo<D>::NC32 : 1];
+    bf16x8 t[QB];   // dims D32.. in lane rows g < TAIL/8, zero elsewhere
 };
 
-// Score tile S^T for the wavefront's 32 queries against the 64 keys of one LDS
+// Score tile S^T for the wavefront's 16 * QB queries against the 64 keys of one LDS
 // stage: S[qb][kb][i] is the score of query (16*qb + lane%16) and key
 // (16*kb + 4*(lane/16) + i) of the tile.
-template <int D>
-__device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, const QFrag<D>& q, Tile& S, int r, int g) {
+template <int D, int QB>
+__device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, const QFrag<D, QB>& q, Tile<QB>& S, int r, int g) {
     using G = Geo<D>;
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) {
@@ -239,7 +243,7 @@ __device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, cons
         u32x4 kt = u32x4{0u, 0u, 0u, 0u};
         if constexpr (G::TAIL > 0) kt = *(const u32x4*)(krow + G::D32 + (8 * g < G::TAIL ? 8 * g : 0));
 #pragma unroll
-        for (int qb = 0; qb < QBW; ++qb) {
+        for (int qb = 0; qb < QB; ++qb) {
             f32x4 s = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int c = 0; c < G::NC32; ++c) s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[c], q.a[qb][c], s, 0, 0, 0);
@@ -251,8 +255,8 @@ __device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, cons
 
 // Online-softmax update of the accumulator with one score tile, then PV.
 // S is taken by value: the mask is applied to a private copy.
-template <int D, int MASK>
-__device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* Vs, int r, int g,
+template <int D, int MASK, int QB>
+__device__ __forceinline__ void accumulate(Acc<D, QB>& acc, Tile<QB> S, const uint16_t* Vs, int r, int g,
                                            int qrow0, int k0, int L, int w, float c) {
     using G = Geo<D>;
     if constexpr (MASK != MASK_NONE) {
@@ -266,7 +270,7 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
         const int jbase = k0 + 4 * g;
         const int lim = L - 1 - jbase;
 #pragma unroll
-        for (int qb = 0; qb < QBW; ++qb) {
+        for (int qb = 0; qb < QB; ++qb) {
             int lo = 0;
             uint32_t span = 0u;
             if constexpr (MASK == MASK_BAND_IN) {
@@ -300,10 +304,10 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
     // the first tiles) are the exact tile maxima formed over the four lanes
     // that share a query, and the queries whose maximum grew by more than
     // the margin are rescaled.  Otherwise every probability is below 2^8.
-    float v[QBW];
+    float v[QB];
     bool hot = false;
 #pragma unroll
-    for (int qb = 0; qb < QBW; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
         v[qb] = NEG_INF;
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
@@ -313,7 +317,7 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
     }
     if (__any(hot)) {
 #pragma unroll
-        for (int qb = 0; qb < QBW; ++qb) {
+        for (int qb = 0; qb < QB; ++qb) {
             const float mx = group_max(v[qb]) * c;
             const float m = acc.thr[qb] == NEG_INF ? NEG_INF : -acc.negm[qb];
             if (mx > m + RESCALE_THRESH) {
@@ -327,9 +331,9 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
         }
     }
     // probabilities, packed to bf16 as the B operand of PV
-    bf16x8 pb[QBW][BK / 32];
+    bf16x8 pb[QB][BK / 32];
 #pragma unroll
-    for (int qb = 0; qb < QBW; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
         const float negm = acc.negm[qb];
         float psum = 0.f;
 #pragma unroll
@@ -365,15 +369,15 @@ __device__ __forceinline__ void accumulate(Acc<D>& acc, Tile S, const uint16_t* 
                 __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(src + 16 * G::VP));
             const bf16x8 va = __builtin_bit_cast(bf16x8, s16x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
 #pragma unroll
-            for (int qb = 0; qb < QBW; ++qb)
+            for (int qb = 0; qb < QB; ++qb)
                 acc.o[qb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[qb][h], acc.o[qb][mb], 0, 0, 0);
         }
     }
 }
 
 // Row sum of one query block, broadcast to every lane of that query.
-template <int D>
-__device__ __forceinline__ float row_sum(const Acc<D>& acc, int qb, int r) {
+template <int D, int QB>
+__device__ __forceinline__ float row_sum(const Acc<D, QB>& acc, int qb, int r) {
     using G = Geo<D>;
     if constexpr (G::ONES) {
         constexpr int MB = D / 16, GS = (D % 16) / 4, IS = (D % 16) % 4;
@@ -443,7 +447,7 @@ __device__ __forceinline__ void issue_tile(const uint16_t* __restrict__ Kbh, con
 }
 
 // Per-workgroup state of the tile walk.
-template <int D>
+template <int D, int QB>
 struct Walk {
     using G = Geo<D>;
     const uint16_t* Kbh;
@@ -458,7 +462,7 @@ struct Walk {
     // tile of the next non-empty segment (-1: none), prefetched while the
     // last tile of this segment is used.
     template <int KIND>
-    __device__ __forceinline__ void run(Acc<D>& acc, const QFrag<D>& q, int t0, int t1, int next_after) {
+    __device__ __forceinline__ void run(Acc<D, QB>& acc, const QFrag<D, QB>& q, int t0, int t1, int next_after) {
         for (int t = t0; t < t1; ++t) {
             const uint16_t* Ks = smem + stage * G::STAGE_ELEMS;
             const uint16_t* Vs = Ks + G::KS_ELEMS;
@@ -475,14 +479,14 @@ struct Walk {
     }
 
     template <int KIND>
-    __device__ __forceinline__ void tile(Acc<D>& acc, const QFrag<D>& q, const uint16_t* Ks, const uint16_t* Vs,
+    __device__ __forceinline__ void tile(Acc<D, QB>& acc, const QFrag<D, QB>& q, const uint16_t* Ks, const uint16_t* Vs,
                                          int k0) {
         if constexpr (KIND == SEG_PLAIN) {
-            Tile S;
+            Tile<QB> S;
             score_tile<D>(Ks, q, S, r, g);
             accumulate<D, MASK_NONE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
         } else if constexpr (KIND == SEG_KEYS) {
-            Tile S;
+            Tile<QB> S;
             score_tile<D>(Ks, q, S, r, g);
             accumulate<D, MASK_KEYS>(acc, S, Vs, r, g, qw0, k0, L, w, c);
         } else {
@@ -494,7 +498,7 @@ struct Walk {
             const int cls = maxd <= w ? TILE_INSIDE : (mind > w ? TILE_OUTSIDE : TILE_BOUNDARY);
             constexpr int SKIP = (KIND == SEG_BAND_IN) ? TILE_OUTSIDE : TILE_INSIDE;
             if (cls == SKIP) return;
-            Tile S;
+            Tile<QB> S;
             score_tile<D>(Ks, q, S, r, g);
             if (cls == TILE_BOUNDARY)
                 accumulate<D, KIND == SEG_BAND_IN ? MASK_BAND_IN : MASK_BAND_OUT>(acc, S, Vs, r, g, qw0, k0, L, w, c);
@@ -506,7 +510,7 @@ struct Walk {
     }
 };
 
-template <int D, int KMODE>
+template <int D, int KMODE, int QB>
 __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     using G = Geo<D>;
     constexpr int MODE = KMODE == MODE_ASC ? MODE_FULL : KMODE;
@@ -528,10 +532,10 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     const size_t head_off = (size_t)bh * L * D;
     const uint16_t* __restrict__ Qbh = p.Q + head_off;
 
-    const int q0 = qt * BQ;                       // workgroup's first query
-    const int qw0 = q0 + wave * (QBW * 16);       // wavefront's first query
-    const int qhi_wg = min(q0 + BQ - 1, L - 1);
-    const int qhi_w = min(qw0 + QBW * 16 - 1, L - 1);
+    const int q0 = qt * bq<QB>();                 // workgroup's first query
+    const int qw0 = q0 + wave * (QB * 16);       // wavefront's first query
+    const int qhi_wg = min(q0 + bq<QB>() - 1, L - 1);
+    const int qhi_w = min(qw0 + QB * 16 - 1, L - 1);
 
     // constant V padding chunk of every row in both stages: (1, 0, ..., 0) for
     // the row-sum column, never overwritten by the tile copies
@@ -543,9 +547,9 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     }
 
     // Q fragments (B operand of S^T = K Q^T), zero beyond L and beyond d
-    QFrag<D> q;
+    QFrag<D, QB> q;
 #pragma unroll
-    for (int qb = 0; qb < QBW; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
         const int qrow = qw0 + 16 * qb + r;
         const bool ok = qrow < L;
         const uint16_t* qp = Qbh + (size_t)(ok ? qrow : 0) * D;
@@ -558,7 +562,7 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
         }
     }
 
-    Walk<D> wk;
+    Walk<D, QB> wk;
     wk.Kbh = p.K + head_off;
     wk.Vbh = p.V + head_off;
     wk.smem = smem;
@@ -613,7 +617,7 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
 #pragma unroll
     for (int i = NSEG - 1; i >= 0; --i) nxt[i] = s0[i] < s1[i] ? s0[i] : nxt[i + 1];
 
-    Acc<D> acc;
+    Acc<D, QB> acc;
     acc.init();
 
     // every workgroup has at least one key tile: the window of any query
@@ -636,7 +640,7 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
         // queries: park W (fp32) in the R buffer
         if (wk.wave_active) {
 #pragma unroll
-            for (int qb = 0; qb < QBW; ++qb) {
+            for (int qb = 0; qb < QB; ++qb) {
                 const int qrow = qw0 + 16 * qb + r;
                 const float inv = 1.f / row_sum<D>(acc, qb, r);
                 if (qrow < L) {
@@ -659,7 +663,7 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
 
     // epilogue: normalise, form R, store bf16 to every destination
 #pragma unroll
-    for (int qb = 0; qb < QBW; ++qb) {
+    for (int qb = 0; qb < QB; ++qb) {
         const int qrow = qw0 + 16 * qb + r;
         const float inv = 1.f / row_sum<D>(acc, qb, r);
         if (qrow >= L) continue;
@@ -689,12 +693,17 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     }
 }
 
-// Three waves per SIMD (register budget 168): the MFMA work of one wavefront
-// overlaps the softmax arithmetic of the others.
-template <int D, int MODE>
-__global__ void __launch_bounds__(NTHREADS) __attribute__((amdgpu_waves_per_eu(3, 3))) attn_kernel(Params p) {
+// Three waves per SIMD with two query blocks per wavefront (register budget
+// 168), four with one (budget 128): the MFMA work of one wavefront overlaps the
+// softmax arithmetic of the others.
+template <int QB>
+constexpr int waves_per_simd() { return QB == 1 ? 4 : 3; }
+
+template <int D, int MODE, int QB>
+__global__ void __launch_bounds__(NTHREADS)
+    __attribute__((amdgpu_waves_per_eu(waves_per_simd<QB>(), waves_per_simd<QB>()))) attn_kernel(Params p) {
     __shared__ __attribute__((aligned(16))) uint16_t smem[2 * Geo<D>::STAGE_ELEMS];
-    attn_body<D, MODE>(p, smem);
+    attn_body<D, MODE, QB>(p, smem);
 }
 
 // Streaming copy of n16 16-byte units (AST output reuse).
@@ -715,7 +724,7 @@ __global__ void __launch_bounds__(256) copy16_kernel(const u32x4* __restrict__ s
     }
 }
 
-template <int D, int MODE>
+template <int D, int MODE, int QB>
 hipError_t launch_attn(const AttnLaunch& a, hipStream_t stream) {
     using G = Geo<D>;
     Params p{};
@@ -729,21 +738,40 @@ hipError_t launch_attn(const AttnLaunch& a, hipStream_t stream) {
     p.H = a.H;
     p.L = a.L;
     p.w = a.w;
-    p.n_qt = (a.L + BQ - 1) / BQ;
+    p.n_qt = (a.L + bq<QB>() - 1) / bq<QB>();
     const long long nb = (long long)p.n_qt * a.B * a.H;
     if (nb <= 0 || nb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
     p.nblocks = (int)nb;
     p.c = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-    static_assert((size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t) * 3 <= 160 * 1024, "three workgroups per CU must fit in LDS");
-    hipLaunchKernelGGL((attn_kernel<D, MODE>), dim3(p.nblocks), dim3(NTHREADS), 0, stream, p);
+    static_assert((size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t) * waves_per_simd<QB>() <= 160 * 1024,
+                  "one workgroup per wave slot of a SIMD must fit in LDS");
+    hipLaunchKernelGGL((attn_kernel<D, MODE, QB>), dim3(p.nblocks), dim3(NTHREADS), 0, stream, p);
     return hipGetLastError();
+}
+
+// One query block per wavefront (64-query workgroups, four wavefronts per
+// SIMD) when a workgroup's tile walk is short: the extra workgroups and
+// wavefronts hide latency there.  Long walks run faster with two blocks,
+// which halve the K/V tile copies per query.  The crossovers, measured at
+// d = 72 with interleaved timings: full attention up to L = 256 (4 key tiles),
+// refresh up to L = 1024, window attention up to a band of 1280 keys.  A band
+// that covers every key is full attention and takes full attention's choice,
+// so that the two give identical results.
+template <int MODE>
+bool one_query_block(const AttnLaunch& a) {
+    if constexpr (MODE == MODE_REFRESH) return a.L <= 1024;
+    if constexpr (MODE == MODE_WINDOW) {
+        if (a.w < a.L - 1) return 2LL * a.w + 1 <= 1280;
+    }
+    return a.L <= 256;
 }
 
 template <int MODE>
 hipError_t launch_mode(const AttnLaunch& a, hipStream_t stream) {
+    const bool one = one_query_block<MODE>(a);
     switch (a.d) {
-        case 64: return launch_attn<64, MODE>(a, stream);
-        case 72: return launch_attn<72, MODE>(a, stream);
+        case 64: return one ? launch_attn<64, MODE, 1>(a, stream) : launch_attn<64, MODE, 2>(a, stream);
+        case 72: return one ? launch_attn<72, MODE, 1>(a, stream) : launch_attn<72, MODE, 2>(a, stream);
         default: return hipErrorInvalidValue;
     }
 }

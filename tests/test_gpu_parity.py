@@ -130,6 +130,27 @@ def test_kernels_vs_oracle(B, H, L, d, w):
         assert torch.equal(O4, O1.t), "a band covering every key must reproduce full attention bitwise"
 
 
+# Launches with short tile walks run 64-query workgroups (one 16-query block
+# per wavefront), longer ones 128-query workgroups; these shapes sit on both
+# sides of each switch: full attention at L = 256, refresh at L = 1024, and
+# window attention at a band of 1280 keys (w = 639 / 640).
+ROUTE_SHAPES = [
+    (1, 2, 256, 72, 32),
+    (1, 2, 257, 64, 32),
+    (2, 1, 1024, 72, 100),
+    (1, 2, 1025, 72, 100),
+    (1, 1, 1500, 64, 639),
+    (1, 1, 1500, 72, 640),
+    (1, 1, 2100, 72, 700),
+    (1, 1, 700, 72, 699),
+]
+
+
+@pytest.mark.parametrize("B,H,L,d,w", ROUTE_SHAPES)
+def test_query_block_routes(B, H, L, d, w):
+    test_kernels_vs_oracle(B, H, L, d, w)
+
+
 def test_long_sequence_sampled():
     """L = 65536 (four times the 2K workload's tokens) through the three
     kernels, on sampled query rows: the first and last rows, the rows at the
