@@ -419,7 +419,7 @@ def main():
         "video": video,
         "reuse_speedup_vs_full": round(kres["full"]["ms"] / kres["wars_reuse"]["ms"], 3),
         "reuse_ideal_speedup": round(L * L / n_band(L, w), 3),
-        "roofline": {"kernel": "attn_kernel<72, FULL> (dfa_attn_full / FULL plan entries)", "bound": "mfma",
+        "roofline": {"kernel": "attn_kernel<72, 0, 2> (full attention, 128-query workgroups: dfa_attn_full / FULL plan entries)", "bound": "mfma",
                      "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic("full", args.workload),
