@@ -25,9 +25,10 @@
 // per k-tile).  Each wavefront owns 64 features x 64 or 128 tokens as blocks
 // of v_mfma_f32_32x32x16_bf16 (operand layouts: lane l, h = l / 32, A element
 // e = A[l % 32][8h + e], B element e = B[8h + e][l % 32], output element
-// i = D[8 (i/4) + 4h + i%4][l % 32]).  LDS rows carry one 16-byte pad chunk
-// (144- or 80-byte pitch), so the 16-byte operand reads of 16 consecutive rows
-// hit distinct bank groups.  Blocks are remapped so that each XCD works
+// i = D[8 (i/4) + 4h + i%4][l % 32]).  The 128-token tile's LDS rows carry one
+// 16-byte pad chunk (144-byte pitch); the 256-token tile's 64-byte rows are
+// swizzled instead (chunk_off).  Either way the staging stores and the 16-byte
+// operand reads are free of bank conflicts.  Blocks are remapped so that each XCD works
 // through a contiguous range of token tiles with all their feature tiles,
 // keeping the token tile's activations in that XCD's L2.
 //
@@ -35,7 +36,9 @@
 // earlier forms of this kernel: scattering 8-byte pieces straight from the
 // accumulators cost about a quarter of the QKV projection's time; direct
 // global->LDS copies were no faster than register staging; the 256-token
-// tile takes about 10% off the QKV projection.  Larger tiles still
+// tile takes about 10% off the QKV projection; its swizzled rows, against
+// 80-byte padded ones, cut LDS bank-conflict cycles from 14% to 1.4% and took
+// 2% more off it.  Larger tiles still
 // (192 x 256 at one wavefront per SIMD, also with a four-stage copy ring)
 // did not beat these shapes.
 #include <hip/hip_runtime.h>
@@ -58,7 +61,7 @@ constexpr int GF = 128;                          // features per workgroup
 constexpr int TILE_FEW = 0, TILE_MANY = 1;       // workgroup tile shapes (see Tile)
 
 // Workgroup tile shape.  TILE_FEW: 128 tokens, k-tiles of 64 (144-byte LDS
-// rows); TILE_MANY: 256 tokens, k-tiles of 32 (80-byte rows), which moves a
+// rows); TILE_MANY: 256 tokens, k-tiles of 32 (64-byte swizzled rows), which moves a
 // quarter fewer bytes into the CUs per FLOP but needs more workgroups to fill
 // the chip.  Both sum over k in the same order, so they give identical results.
 template <int SHAPE>
@@ -67,7 +70,8 @@ struct Tile {
     static constexpr int GTOK = 64 * BT;                       // tokens per workgroup
     static constexpr int GK = SHAPE == TILE_MANY ? 32 : 64;    // k per LDS tile
     static constexpr int GCH = GK / 8;                         // 16-byte chunks of data per row
-    static constexpr int GP = (GCH + 1) * 8;                   // row pitch in elements (one pad chunk)
+    static constexpr bool SWZ = SHAPE == TILE_MANY;            // swizzled 64-byte rows instead of a pad chunk
+    static constexpr int GP = (GCH + (SWZ ? 0 : 1)) * 8;       // row pitch in elements
     static constexpr int ATILE = GF * GP;                      // W tile
     static constexpr int STAGE = (GF + GTOK) * GP;             // W tile, then activation tile
     static constexpr int OP = GF + 8;                          // output staging row pitch (elements)
@@ -77,6 +81,19 @@ struct Tile {
     static_assert(GF * GCH % GT == 0 && GTOK * GCH % GT == 0, "chunks per thread");
     static_assert((size_t)SMEM * sizeof(uint16_t) * 2 <= 160 * 1024, "two workgroups per CU must fit in LDS");
 };
+
+// Element offset of 16-byte chunk ch of LDS row row.  Padded rows keep the
+// chunk in place.  Swizzled rows (four chunks, 64 bytes) move it to
+// ch ^ s(row), s(row) = bits 2-3 of row in reverse order: the staging stores
+// (whole rows) and the operand reads (one chunk of 32 consecutive rows per
+// half-wavefront) then both fall on distinct bank groups, where a 16-byte pad
+// on 64-byte rows leaves the stores with conflicts.
+template <int SHAPE>
+__device__ __forceinline__ int chunk_off(int row, int ch) {
+    using T = Tile<SHAPE>;
+    if constexpr (T::SWZ) return row * T::GP + ((ch ^ (((row >> 1) & 2) | ((row >> 3) & 1))) << 3);
+    return row * T::GP + ch * 8;
+}
 
 enum { ACT_ROWS = 0, ACT_HEADS = 1 };   // activations: [M][K] rows, or O [B][H][L][d]
 enum { OUT_QKV = 0, OUT_ROWS = 1 };     // epilogue: scatter to Q/K/V, or [M][N] rows
@@ -136,12 +153,12 @@ __device__ __forceinline__ void store_gemm_tile(int tid, const u32x4 (&r)[Tile<S
 #pragma unroll
     for (int it = 0; it < T::ACH; ++it) {
         const int c = it * GT + tid;
-        *(u32x4*)(As + (c / T::GCH) * T::GP + (c % T::GCH) * 8) = r[it];
+        *(u32x4*)(As + chunk_off<SHAPE>(c / T::GCH, c % T::GCH)) = r[it];
     }
 #pragma unroll
     for (int it = 0; it < T::BCH; ++it) {
         const int c = it * GT + tid;
-        *(u32x4*)(Bs + (c / T::GCH) * T::GP + (c % T::GCH) * 8) = r[T::ACH + it];
+        *(u32x4*)(Bs + chunk_off<SHAPE>(c / T::GCH, c % T::GCH)) = r[T::ACH + it];
     }
 }
 
@@ -179,15 +196,17 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
         const uint16_t* As = smem + stage * T::STAGE;
         const uint16_t* Bs = As + T::ATILE;
         if (kt + 1 < nk) load_gemm_tile<ACT, SHAPE>(p, n0, t0, kt + 1, tid, stg);
-        const uint16_t* arow = As + (64 * wf + r32) * GP + 8 * h;
-        const uint16_t* brow = Bs + (32 * BT * wt + r32) * GP + 8 * h;
 #pragma unroll
         for (int ks = 0; ks < GK / 16; ++ks) {
+            // operand rows differ from the lane's first row by multiples of 32,
+            // which leave the swizzle unchanged
+            const uint16_t* arow = As + chunk_off<SHAPE>(64 * wf + r32, 2 * ks + h);
+            const uint16_t* brow = Bs + chunk_off<SHAPE>(32 * BT * wt + r32, 2 * ks + h);
             bf16x8 a[2], b[BT];
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb) a[mb] = __builtin_bit_cast(bf16x8, *(const u32x4*)(arow + 32 * mb * GP + 16 * ks));
+            for (int mb = 0; mb < 2; ++mb) a[mb] = __builtin_bit_cast(bf16x8, *(const u32x4*)(arow + 32 * mb * GP));
 #pragma unroll
-            for (int nb = 0; nb < BT; ++nb) b[nb] = __builtin_bit_cast(bf16x8, *(const u32x4*)(brow + 32 * nb * GP + 16 * ks));
+            for (int nb = 0; nb < BT; ++nb) b[nb] = __builtin_bit_cast(bf16x8, *(const u32x4*)(brow + 32 * nb * GP));
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
