@@ -85,10 +85,12 @@ constexpr int bq() { return NWAVES * QB * 16; }
 constexpr float RESCALE_THRESH = 8.0f;    // lazy rescale margin (log2 units)
 constexpr float NEG_INF = -__builtin_inff();
 
-enum { MODE_FULL = 0, MODE_REFRESH = 1, MODE_WINDOW = 2, MODE_ASC = 3 };
+enum { MODE_FULL = 0, MODE_REFRESH = 1, MODE_WINDOW = 2, MODE_ASC = 3, MODE_REFRESH_SPLIT = 4 };
 // MODE_ASC computes exactly what MODE_FULL computes (on the conditional half of
 // the batch, storing every tile to both halves); it is a separate
 // instantiation only so that profiles report it apart from full attention.
+// MODE_REFRESH_SPLIT computes what MODE_REFRESH computes, in one pass with two
+// accumulators instead of two phases with one (short sequences).
 enum { MASK_NONE = 0, MASK_KEYS = 1, MASK_BAND_IN = 2, MASK_BAND_OUT = 3 };
 enum { TILE_INSIDE = 0, TILE_OUTSIDE = 1, TILE_BOUNDARY = 2 };
 // segment kinds of the tile walk
@@ -478,6 +480,50 @@ struct Walk {
         }
     }
 
+    // Single pass over tiles [t0, t1) with two accumulators: the in-band
+    // scores of each tile go to aw, the out-of-band ones to ax.  A tile that
+    // is inside or outside the band for all of the wavefront's queries feeds
+    // one of them; a band-edge tile is scored once and feeds both.
+    __device__ __forceinline__ void run_split(Acc<D, QB>& aw, Acc<D, QB>& ax, const QFrag<D, QB>& q, int t0, int t1) {
+        for (int t = t0; t < t1; ++t) {
+            const uint16_t* Ks = smem + stage * G::STAGE_ELEMS;
+            const uint16_t* Vs = Ks + G::KS_ELEMS;
+            if (t + 1 < t1) {
+                uint16_t* Kn = smem + (stage ^ 1) * G::STAGE_ELEMS;
+                issue_tile<D>(Kbh, Vbh, (t + 1) * BK, L, tid, Kn, Kn + G::KS_ELEMS);
+            }
+            if (wave_active) tile_split(aw, ax, q, Ks, Vs, t * BK);
+            wait_vm_all();
+            __syncthreads();
+            stage ^= 1;
+        }
+    }
+
+    __device__ __forceinline__ int classify(int k0) const {
+        const int khi = min(k0 + BK - 1, L - 1);
+        const int mind = khi < qw0 ? qw0 - khi : (k0 > qhi_w ? k0 - qhi_w : 0);
+        const int maxd = max(qhi_w - k0, khi - qw0);
+        return maxd <= w ? TILE_INSIDE : (mind > w ? TILE_OUTSIDE : TILE_BOUNDARY);
+    }
+
+    __device__ __forceinline__ void tile_split(Acc<D, QB>& aw, Acc<D, QB>& ax, const QFrag<D, QB>& q,
+                                               const uint16_t* Ks, const uint16_t* Vs, int k0) {
+        const bool ragged = k0 + BK > L;
+        const int cls = classify(k0);
+        Tile<QB> S;
+        score_tile<D>(Ks, q, S, r, g);
+        if (cls == TILE_BOUNDARY) {
+            accumulate<D, MASK_BAND_IN>(aw, S, Vs, r, g, qw0, k0, L, w, c);
+            accumulate<D, MASK_BAND_OUT>(ax, S, Vs, r, g, qw0, k0, L, w, c);
+        } else if (cls == TILE_INSIDE) {
+            if (ragged) accumulate<D, MASK_KEYS>(aw, S, Vs, r, g, qw0, k0, L, w, c);
+            else accumulate<D, MASK_NONE>(aw, S, Vs, r, g, qw0, k0, L, w, c);
+        } else {
+            if (ragged) accumulate<D, MASK_KEYS>(ax, S, Vs, r, g, qw0, k0, L, w, c);
+            else accumulate<D, MASK_NONE>(ax, S, Vs, r, g, qw0, k0, L, w, c);
+        }
+    }
+
     template <int KIND>
     __device__ __forceinline__ void tile(Acc<D, QB>& acc, const QFrag<D, QB>& q, const uint16_t* Ks, const uint16_t* Vs,
                                          int k0) {
@@ -492,10 +538,7 @@ struct Walk {
         } else {
             // classify the tile against this wavefront's queries
             const bool ragged = k0 + BK > L;
-            const int khi = min(k0 + BK - 1, L - 1);
-            const int mind = khi < qw0 ? qw0 - khi : (k0 > qhi_w ? k0 - qhi_w : 0);
-            const int maxd = max(qhi_w - k0, khi - qw0);
-            const int cls = maxd <= w ? TILE_INSIDE : (mind > w ? TILE_OUTSIDE : TILE_BOUNDARY);
+            const int cls = classify(k0);
             constexpr int SKIP = (KIND == SEG_BAND_IN) ? TILE_OUTSIDE : TILE_INSIDE;
             if (cls == SKIP) return;
             Tile<QB> S;
@@ -510,10 +553,60 @@ struct Walk {
     }
 };
 
+template <int KMODE>
+constexpr bool split_refresh() { return KMODE == MODE_REFRESH_SPLIT; }
+
+// Refresh in one pass (Sec. 3.2, Eq. 1), for short sequences: W = aw / lw from the in-band scores
+// alone; O combines both accumulators, each scaled from its own running max
+// to the larger one.  A query whose band covers every key has no
+// out-of-band score, and its O is then formed exactly as W, so R == 0.
+template <int D, int QB>
+__device__ __forceinline__ void refresh_split(const Params& p, uint16_t* smem, Walk<D, QB>& wk, const QFrag<D, QB>& q,
+                                              size_t head_off, int ntiles) {
+    using G = Geo<D>;
+    Acc<D, QB> aw, ax;
+    aw.init();
+    ax.init();
+    issue_tile<D>(wk.Kbh, wk.Vbh, 0, wk.L, wk.tid, smem, smem + G::KS_ELEMS);
+    wait_vm_all();
+    __syncthreads();
+    wk.run_split(aw, ax, q, 0, ntiles);
+    if (!wk.wave_active) return;
+    const int r = wk.r, g = wk.g;
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+        const int qrow = wk.qw0 + 16 * qb + r;
+        // row sums first: they exchange values across lanes
+        const float lw = row_sum<D>(aw, qb, r), lx = row_sum<D>(ax, qb, r);
+        const bool has_x = ax.thr[qb] != NEG_INF;
+        const float mw = aw.thr[qb] == NEG_INF ? NEG_INF : -aw.negm[qb];
+        const float mx = has_x ? -ax.negm[qb] : NEG_INF;
+        const float mm = fmaxf(mw, mx);
+        const float sw = has_x ? __builtin_amdgcn_exp2f(mw - mm) : 1.f;
+        const float sx = has_x ? __builtin_amdgcn_exp2f(mx - mm) : 0.f;
+        const float invw = 1.f / lw;
+        const float inv = 1.f / (lw * sw + lx * sx);
+        if (qrow >= wk.L) continue;
+        const size_t row_off = head_off + (size_t)qrow * D;
+#pragma unroll
+        for (int mb = 0; mb < G::NDB; ++mb) {
+#pragma clang fp contract(off)
+            const int col = 16 * mb + 4 * g;
+            if (col >= D) continue;
+            const size_t off = row_off + col;
+            const f32x4 wv = aw.o[qb][mb] * invw;
+            const f32x4 o = has_x ? (aw.o[qb][mb] * sw + ax.o[qb][mb] * sx) * inv : wv;
+            *(f32x4*)(p.Rout + off) = o - wv;
+            const u32x2 ov = u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+            for (int di = 0; di < p.ndst; ++di) *(u32x2*)(p.dst[di] + off) = ov;
+        }
+    }
+}
+
 template <int D, int KMODE, int QB>
 __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     using G = Geo<D>;
-    constexpr int MODE = KMODE == MODE_ASC ? MODE_FULL : KMODE;
+    constexpr int MODE = KMODE == MODE_ASC ? MODE_FULL : (KMODE == MODE_REFRESH_SPLIT ? MODE_REFRESH : KMODE);
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -617,6 +710,11 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
 #pragma unroll
     for (int i = NSEG - 1; i >= 0; --i) nxt[i] = s0[i] < s1[i] ? s0[i] : nxt[i + 1];
 
+    if constexpr (split_refresh<KMODE>()) {
+        refresh_split<D, QB>(p, smem, wk, q, head_off, ntiles);
+        return;
+    }
+
     Acc<D, QB> acc;
     acc.init();
 
@@ -694,14 +792,14 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
 }
 
 // Three waves per SIMD with two query blocks per wavefront (register budget
-// 168), four with one (budget 128): the MFMA work of one wavefront overlaps the
-// softmax arithmetic of the others.
-template <int QB>
-constexpr int waves_per_simd() { return QB == 1 ? 4 : 3; }
+// 168), four with one (budget 128), three for the two-accumulator refresh: the
+// MFMA work of one wavefront overlaps the softmax arithmetic of the others.
+template <int QB, int KMODE>
+constexpr int waves_per_simd() { return QB == 1 && !split_refresh<KMODE>() ? 4 : 3; }
 
 template <int D, int MODE, int QB>
 __global__ void __launch_bounds__(NTHREADS)
-    __attribute__((amdgpu_waves_per_eu(waves_per_simd<QB>(), waves_per_simd<QB>()))) attn_kernel(Params p) {
+    __attribute__((amdgpu_waves_per_eu(waves_per_simd<QB, MODE>(), waves_per_simd<QB, MODE>()))) attn_kernel(Params p) {
     __shared__ __attribute__((aligned(16))) uint16_t smem[2 * Geo<D>::STAGE_ELEMS];
     attn_body<D, MODE, QB>(p, smem);
 }
@@ -743,7 +841,7 @@ hipError_t launch_attn(const AttnLaunch& a, hipStream_t stream) {
     if (nb <= 0 || nb > 0x7FFFFFFFLL) return hipErrorInvalidValue;
     p.nblocks = (int)nb;
     p.c = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-    static_assert((size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t) * waves_per_simd<QB>() <= 160 * 1024,
+    static_assert((size_t)2 * G::STAGE_ELEMS * sizeof(uint16_t) * waves_per_simd<QB, MODE>() <= 160 * 1024,
                   "one workgroup per wave slot of a SIMD must fit in LDS");
     hipLaunchKernelGGL((attn_kernel<D, MODE, QB>), dim3(p.nblocks), dim3(NTHREADS), 0, stream, p);
     return hipGetLastError();
@@ -759,7 +857,7 @@ hipError_t launch_attn(const AttnLaunch& a, hipStream_t stream) {
 // so that the two give identical results.
 template <int MODE>
 bool one_query_block(const AttnLaunch& a) {
-    if constexpr (MODE == MODE_REFRESH) return a.L <= 1024;
+    if constexpr (MODE == MODE_REFRESH) return a.L <= 1024;   // L <= 512 takes the split form
     if constexpr (MODE == MODE_WINDOW) {
         if (a.w < a.L - 1) return 2LL * a.w + 1 <= 1280;
     }
@@ -782,7 +880,17 @@ bool head_dim_supported(int d) { return d == 64 || d == 72; }
 
 hipError_t launch_full(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_FULL>(a, s); }
 hipError_t launch_asc(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_ASC>(a, s); }
-hipError_t launch_refresh(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_REFRESH>(a, s); }
+// Refresh: the one-pass two-accumulator form up to L = 512 (8 key tiles, where
+// band-edge tiles are most of the walk), the two-phase form beyond (measured:
+// L = 256 -16%, 405 -6%, 1024 +3% for the one-pass form).
+hipError_t launch_refresh(const AttnLaunch& a, hipStream_t s) {
+    if (a.L > 512) return launch_mode<MODE_REFRESH>(a, s);
+    switch (a.d) {
+        case 64: return launch_attn<64, MODE_REFRESH_SPLIT, 1>(a, s);
+        case 72: return launch_attn<72, MODE_REFRESH_SPLIT, 1>(a, s);
+        default: return hipErrorInvalidValue;
+    }
+}
 hipError_t launch_window(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_WINDOW>(a, s); }
 
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {

@@ -132,10 +132,13 @@ def test_kernels_vs_oracle(B, H, L, d, w):
 
 # Launches with short tile walks run 64-query workgroups (one 16-query block
 # per wavefront), longer ones 128-query workgroups; these shapes sit on both
-# sides of each switch: full attention at L = 256, refresh at L = 1024, and
-# window attention at a band of 1280 keys (w = 639 / 640).
+# sides of each switch: full attention at L = 256, refresh at L = 512 (one
+# pass with two accumulators up to there) and at L = 1024, and window
+# attention at a band of 1280 keys (w = 639 / 640).
 ROUTE_SHAPES = [
     (1, 2, 256, 72, 32),
+    (1, 2, 512, 64, 40),
+    (2, 1, 513, 72, 40),
     (1, 2, 257, 64, 32),
     (2, 1, 1024, 72, 100),
     (1, 2, 1025, 72, 100),
@@ -226,7 +229,9 @@ def test_concurrent_streams_match_serial():
 
 
 @pytest.mark.parametrize("kind,L,d,w", [("large", 2048, 72, 300), ("growing", 2048, 72, 300),
-                                         ("growing", 1000, 64, 77), ("large", 777, 64, 0)])
+                                         ("growing", 1000, 64, 77), ("large", 777, 64, 0),
+                                         ("growing", 500, 72, 40), ("large", 300, 64, 0),
+                                         ("growing", 200, 72, 199)])
 def test_rescale_paths(kind, L, d, w):
     """Inputs that drive the online softmax's rescale: scores of large spread
     (Q and K scaled by 6, nearly one-hot rows), or scores that grow along the
