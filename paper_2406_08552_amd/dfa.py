@@ -96,27 +96,48 @@ def _ptr(t) -> int | None:
     return None if t is None else t.data_ptr()
 
 
+_TORCH = None
+_RAW_STREAM = None
+
+
+def _torch():
+    """torch, imported on first use (the ABI tests run without a GPU)."""
+    global _TORCH, _RAW_STREAM
+    if _TORCH is None:
+        import torch
+        _TORCH = torch
+        _RAW_STREAM = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+    return _TORCH
+
+
 def _shape(*tensors, R=None):
-    import torch
+    torch = _torch()
     ref = tensors[0]
+    shape = ref.shape
+    bf16, f32 = torch.bfloat16, torch.float32
     for t in (*tensors, R):
         if t is None:
             continue
-        want = torch.float32 if t is R else torch.bfloat16
+        want = f32 if t is R else bf16
         if t.dtype != want:
             raise TypeError(f"expected {want} (R is fp32, the rest bf16), got {t.dtype}")
         if not t.is_contiguous():
             raise ValueError("tensors must be contiguous [B, H, L, d]")
-        if t.device.type != "cuda":
+        if not t.is_cuda:
             raise ValueError("tensors must live on a GPU")
-        if t.shape != ref.shape or t.dim() != 4:
-            raise ValueError(f"shape mismatch: {tuple(t.shape)} vs {tuple(ref.shape)}")
-    return tuple(ref.shape)
+        if t.shape != shape or t.dim() != 4:
+            raise ValueError(f"shape mismatch: {tuple(t.shape)} vs {tuple(shape)}")
+    return tuple(shape)
 
 
 def _stream(stream) -> int:
-    import torch
+    """The HIP stream handle of `stream`, or of torch's current stream.  The
+    raw query returns the same handle as torch.cuda.current_stream() without
+    building a Stream object (a few microseconds per call)."""
+    torch = _torch()
     if stream is None:
+        if _RAW_STREAM is not None:
+            return _RAW_STREAM(torch.cuda.current_device())
         stream = torch.cuda.current_stream()
     return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
 
@@ -149,10 +170,9 @@ def dfa_plan_step(code: int, Q, K, V, O, R, Ocache, w: int, stream=None) -> None
 
 
 def _expect(t, dtype, shape, name):
-    import torch
     if t is None:
         return
-    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or t.device.type != "cuda":
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or not t.is_cuda:
         raise ValueError(f"{name}: expected a contiguous {dtype} GPU tensor of shape {tuple(shape)}, "
                          f"got {t.dtype} {tuple(t.shape)} on {t.device}")
 
