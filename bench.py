@@ -118,6 +118,38 @@ def video_bench(args, dfa, inputs, torch, dev, stream):
     return out
 
 
+def shape_sweep(dfa, inputs, torch, dev, stream):
+    """Full attention, WA-RS refresh and WA-RS reuse at every d = 72 workload
+    shape (DiT-XL/2 256 and 512 px, PixArt-Sigma 1K and 2K): a warm-up, then
+    the median over five rounds of back-to-back launches (HIP events on the
+    launch stream).  TFLOP/s counts each entry's algorithmic FLOPs."""
+    import statistics
+    out = {}
+    for key in ("dit256", "dit512", "pixart1k", "pixart2k"):
+        cfg = inputs.CONFIGS[key]
+        B, H, L, d, w = cfg.B, cfg.H, cfg.L, cfg.d, cfg.w
+        shape = (B, H, L, d)
+        q, k, v = inputs.device_qkv(inputs.SEED_BASE + 8000 + cfg.cfg_id, shape, dev)
+        O = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+        R = torch.empty(shape, dtype=torch.float32, device=dev)
+        full = 4.0 * B * H * L * L * d
+        band = 4.0 * B * H * d * n_band(L, w)
+        runs = {
+            "full": (lambda: dfa.dfa_attn_full(q, k, v, O, w, stream), full),
+            "wars_refresh": (lambda: dfa.dfa_attn_full_and_residual(q, k, v, O, R, w, stream), full),
+            "wars_reuse": (lambda: dfa.dfa_attn_window_plus_residual(q, k, v, O, R, w, stream), band),
+        }
+        reps = 5 if L > 8192 else 50
+        res = {"B": B, "H": H, "L": L, "d": d, "w": w}
+        for name, (fn, fl) in runs.items():
+            timed(torch, stream, fn, reps)
+            ms = statistics.median(timed(torch, stream, fn, reps) for _ in range(5))
+            res[name] = {"ms": round(ms, 5), "tflops": round(fl / (ms * 1e-3) / 1e12, 1)}
+        res["reuse_over_full"] = round(res["wars_reuse"]["ms"] / res["full"]["ms"], 4)
+        out[cfg.name] = res
+    return out
+
+
 def search_bench(args, dfa, inputs, torch, dev, stream):
     """The greedy plan search (Alg. 1) on a 28-layer surrogate of DiT-XL/2 at
     512 px (B = 8 as four CFG pairs, L = 1024, H = 16, d = 72, band half-width
@@ -221,6 +253,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--search-steps", type=int, default=3, help="denoising steps of the plan-search measurement")
     ap.add_argument("--search-delta", type=float, default=0.1)
+    ap.add_argument("--shape-sweep", action="store_true",
+                    help="instead of the benchmark, time full / refresh / reuse at every d = 72 workload shape")
     return ap.parse_args()
 
 
@@ -268,6 +302,12 @@ def main():
     import torch
 
     from paper_2406_08552_amd import dfa, inputs
+
+    if args.shape_sweep:
+        dev = torch.device("cuda:0")
+        stream = torch.cuda.current_stream(dev)
+        print(json.dumps({"shape_sweep": shape_sweep(dfa, inputs, torch, dev, stream)}), flush=True)
+        return
 
     cfg = inputs.CONFIGS[args.workload]
     B, H, L, d, w = cfg.B, cfg.H, cfg.L, cfg.d, cfg.w
