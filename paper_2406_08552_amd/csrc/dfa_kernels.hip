@@ -49,16 +49,18 @@
 //   The key tiles a workgroup visits are split into segments so that the hot
 //   loop carries no mask: tiles where every score counts (PLAIN), the ragged
 //   last tile (KEYS: j < L), and the tiles at the band edges, where each
-//   wavefront classifies the tile against its own 32 queries (inside the
-//   band, outside, or straddling it with an element mask).
+//   wavefront classifies the tile against its own queries (inside the band,
+//   outside, or straddling it with an element mask).
 //   The window kernel visits only the tiles that intersect the workgroup's
-//   band.  The refresh kernel runs ONE accumulator over two phases: first
-//   the in-band scores of the band tiles (after which the accumulator,
-//   normalised, is the window attention W; it is parked in the R buffer),
-//   then every out-of-band score, which turns the same accumulator into full
-//   attention.  R = O - W is formed in the epilogue.  Every score is used
-//   exactly once, only the few band-edge tiles are visited twice, and no
-//   second accumulator occupies registers.
+//   band.  For L > 512 the refresh kernel runs ONE accumulator over two
+//   phases: first the in-band scores of the band tiles (after which the
+//   accumulator, normalised, is the window attention W; it is parked in the R
+//   buffer), then every out-of-band score, which turns the same accumulator
+//   into full attention.  R = O - W is formed in the epilogue.  Every score is
+//   used exactly once, only the few band-edge tiles are visited twice, and no
+//   second accumulator occupies registers.  Up to L = 512, where band-edge
+//   tiles are most of the walk, the refresh instead keeps two accumulators
+//   and visits every tile once (MODE_REFRESH_SPLIT).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
