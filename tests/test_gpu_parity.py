@@ -192,21 +192,25 @@ def test_concurrent_streams_match_serial():
     shape_a, shape_b = (2, 4, 1024, 72), (1, 8, 777, 64)
     qa, ka, va = (t.to(dev) for t in rand_qkv(shape_a, 91))
     qb, kb, vb = (t.to(dev) for t in rand_qkv(shape_b, 92))
-    say("two streams: refresh + reuse on one, full + short-sequence on the other")
+    say("two streams: refresh + reuse on one, full + short-sequence + one-pass refresh on the other")
     qs, ks, vs = (t.to(dev) for t in rand_qkv((8, 16, 16, 72), 93))
+    shape_c = (1, 4, 400, 72)
+    qc, kc, vc = (t.to(dev) for t in rand_qkv(shape_c, 94))
 
     def work(outs):
-        Oa, Ra, Oa2, Ob, Os = outs
+        Oa, Ra, Oa2, Ob, Os, Oc, Rc = outs
         return [lambda: dfa.dfa_attn_full_and_residual(qa, ka, va, Oa, Ra, 128),
                 lambda: dfa.dfa_attn_window_plus_residual(qa, ka, va, Oa2, Ra, 128),
                 lambda: dfa.dfa_attn_full(qb, kb, vb, Ob, 0),
                 lambda: dfa.dfa_plan_step(dfa.WARS_REFRESH, qs, ks, vs, Os, torch.empty(qs.shape, dtype=torch.float32,
-                                                                                        device=dev), None, 2)]
+                                                                                        device=dev), None, 2),
+                lambda: dfa.dfa_attn_full_and_residual(qc, kc, vc, Oc, Rc, 40)]
 
     def fresh():
         return (torch.empty(shape_a, dtype=torch.bfloat16, device=dev), torch.empty(shape_a, dtype=torch.float32, device=dev),
                 torch.empty(shape_a, dtype=torch.bfloat16, device=dev), torch.empty(shape_b, dtype=torch.bfloat16, device=dev),
-                torch.empty(qs.shape, dtype=torch.bfloat16, device=dev))
+                torch.empty(qs.shape, dtype=torch.bfloat16, device=dev),
+                torch.empty(shape_c, dtype=torch.bfloat16, device=dev), torch.empty(shape_c, dtype=torch.float32, device=dev))
 
     serial = fresh()
     for f in work(serial):
