@@ -130,12 +130,17 @@ def test_kernels_vs_oracle(B, H, L, d, w):
         assert torch.equal(O4, O1.t), "a band covering every key must reproduce full attention bitwise"
 
 
-# Launches with short tile walks run 64-query workgroups (one 16-query block
-# per wavefront), longer ones 128-query workgroups; these shapes sit on both
-# sides of each switch: full attention at L = 256, refresh at L = 512 (one
-# pass with two accumulators up to there) and at L = 1024, and window
-# attention at a band of 1280 keys (w = 639 / 640).
+# Launches with short tile walks, or with at most 256 workgroups of 128
+# queries, run 64-query workgroups (one 16-query block per wavefront), the
+# rest 128-query workgroups; these shapes sit on both sides of each switch:
+# full attention at L = 256, refresh at L = 512 (one pass with two
+# accumulators up to there) and at L = 1024, window attention at a band of
+# 1280 keys (w = 639 / 640), and the workgroup count (B*H*ceil(L/128) = 256
+# against 288 and 384).
 ROUTE_SHAPES = [
+    (1, 16, 2048, 72, 256),
+    (2, 16, 1025, 72, 100),
+    (2, 16, 1500, 64, 640),
     (1, 2, 256, 72, 32),
     (1, 2, 512, 64, 40),
     (2, 1, 513, 72, 40),
