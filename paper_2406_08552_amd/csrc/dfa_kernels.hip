@@ -4,6 +4,7 @@
 //   MODE_FULL     O = softmax(Q K^T / sqrt(d)) V                 (Sec. 3.2, Eq. 1 first line)
 //   MODE_REFRESH  O = full attention, R = O - window attention    (Sec. 3.2, Eq. 1), R in fp32
 //   MODE_WINDOW   O = window attention (+ R when given)           (Sec. 3.2, Eq. 2)
+//   MODE_WINDOW_FINE  the same for bands of at most 31 keys, with split probabilities
 // The window is the band |i - j| <= w over the flattened token index.
 //
 // Work decomposition
@@ -45,6 +46,14 @@
 //   its own scores against that threshold; the exact maxima across lanes are
 //   formed only inside the rare rescale branch.
 //
+// Narrow bands
+//   A bf16 probability is off by up to 2^-8 of itself.  Over many keys these
+//   errors average out; over a band of a few keys they do not, and the output
+//   moves by up to 2^-8 max|v - o| on top of its own bf16 rounding.  Bands of
+//   at most 31 keys per query therefore apply each probability twice: as its
+//   bf16 value and as the bf16 rounding of its residual p - bf16(p), in two PV
+//   products, so each weight is applied to about 2^-16 relative.
+//
 // Tile walk and band handling
 //   The key tiles a workgroup visits are split into segments so that the hot
 //   loop carries no mask: tiles where every score counts (PLAIN), the ragged
@@ -85,9 +94,10 @@ constexpr int NKB = BK / 16;              // 16-key blocks per tile
 template <int QB>
 constexpr int bq() { return NWAVES * QB * 16; }
 constexpr float RESCALE_THRESH = 8.0f;    // lazy rescale margin (log2 units)
+constexpr int FINE_MAX_HALF_WIDTH = 15;   // window half-widths applied with split probabilities
 constexpr float NEG_INF = -__builtin_inff();
 
-enum { MODE_FULL = 0, MODE_REFRESH = 1, MODE_WINDOW = 2, MODE_ASC = 3, MODE_REFRESH_SPLIT = 4 };
+enum { MODE_FULL = 0, MODE_REFRESH = 1, MODE_WINDOW = 2, MODE_ASC = 3, MODE_REFRESH_SPLIT = 4, MODE_WINDOW_FINE = 5 };
 // MODE_ASC computes exactly what MODE_FULL computes (on the conditional half of
 // the batch, storing every tile to both halves); it is a separate
 // instantiation only so that profiles report it apart from full attention.
@@ -156,6 +166,12 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 __device__ __forceinline__ float pair_acc(uint32_t w, float acc) {
     const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, acc, false);
+}
+
+// The rounding residuals lo - bf16(lo) and hi - bf16(hi) of a pair packed by
+// pack_bf16x2 (exact in fp32), themselves packed to bf16.
+__device__ __forceinline__ uint32_t pack_residual(float lo, float hi, uint32_t packed) {
+    return pack_bf16x2(lo - __builtin_bit_cast(float, packed << 16), hi - __builtin_bit_cast(float, packed & 0xFFFF0000u));
 }
 
 // s_waitcnt vmcnt(0): every global access of this wavefront has completed.
@@ -259,7 +275,7 @@ __device__ __forceinline__ void score_tile(const uint16_t* __restrict__ Ks, cons
 
 // Online-softmax update of the accumulator with one score tile, then PV.
 // S is taken by value: the mask is applied to a private copy.
-template <int D, int MASK, int QB>
+template <int D, int MASK, int QB, bool FINE = false>
 __device__ __forceinline__ void accumulate(Acc<D, QB>& acc, Tile<QB> S, const uint16_t* Vs, int r, int g,
                                            int qrow0, int k0, int L, int w, float c) {
     using G = Geo<D>;
@@ -334,15 +350,19 @@ __device__ __forceinline__ void accumulate(Acc<D, QB>& acc, Tile<QB> S, const ui
             }
         }
     }
-    // probabilities, packed to bf16 as the B operand of PV
+    // probabilities, packed to bf16 as the B operand of PV.  FINE adds a
+    // second operand, the rounding residual p - bf16(p) rounded to bf16, so
+    // that the two PV products apply each weight to about 2^-16 relative:
+    // rows with few keys do not average the bf16 rounding of their weights.
     bf16x8 pb[QB][BK / 32];
+    [[maybe_unused]] bf16x8 pl[FINE ? QB : 1][BK / 32];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
         const float negm = acc.negm[qb];
         float psum = 0.f;
 #pragma unroll
         for (int h = 0; h < BK / 32; ++h) {
-            uint32_t wds[4];
+            uint32_t wds[4], rws[4];
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
                 const f32x4 s = S.s[qb][2 * h + half];
@@ -352,9 +372,17 @@ __device__ __forceinline__ void accumulate(Acc<D, QB>& acc, Tile<QB> S, const ui
                 const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[3], c, negm));
                 wds[2 * half + 0] = pack_bf16x2(p0, p1);
                 wds[2 * half + 1] = pack_bf16x2(p2, p3);
-                if constexpr (!G::ONES) psum = pair_acc(wds[2 * half + 1], pair_acc(wds[2 * half], psum));
+                if constexpr (FINE) {
+                    rws[2 * half + 0] = pack_residual(p0, p1, wds[2 * half + 0]);
+                    rws[2 * half + 1] = pack_residual(p2, p3, wds[2 * half + 1]);
+                }
+                if constexpr (!G::ONES) {
+                    psum = pair_acc(wds[2 * half + 1], pair_acc(wds[2 * half], psum));
+                    if constexpr (FINE) psum = pair_acc(rws[2 * half + 1], pair_acc(rws[2 * half], psum));
+                }
             }
             pb[qb][h] = as_bf16x8(u32x4{wds[0], wds[1], wds[2], wds[3]});
+            if constexpr (FINE) pl[qb][h] = as_bf16x8(u32x4{rws[0], rws[1], rws[2], rws[3]});
         }
         if constexpr (!G::ONES) acc.l[qb] += psum;
     }
@@ -373,8 +401,11 @@ __device__ __forceinline__ void accumulate(Acc<D, QB>& acc, Tile<QB> S, const ui
                 __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(src + 16 * G::VP));
             const bf16x8 va = __builtin_bit_cast(bf16x8, s16x8{v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]});
 #pragma unroll
-            for (int qb = 0; qb < QB; ++qb)
+            for (int qb = 0; qb < QB; ++qb) {
                 acc.o[qb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pb[qb][h], acc.o[qb][mb], 0, 0, 0);
+                if constexpr (FINE)
+                    acc.o[qb][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, pl[qb][h], acc.o[qb][mb], 0, 0, 0);
+            }
         }
     }
 }
@@ -465,7 +496,7 @@ struct Walk {
     // Visit tiles [t0, t1) with one segment kind; `next_after` is the first
     // tile of the next non-empty segment (-1: none), prefetched while the
     // last tile of this segment is used.
-    template <int KIND>
+    template <int KIND, bool FINE = false>
     __device__ __forceinline__ void run(Acc<D, QB>& acc, const QFrag<D, QB>& q, int t0, int t1, int next_after) {
         for (int t = t0; t < t1; ++t) {
             const uint16_t* Ks = smem + stage * G::STAGE_ELEMS;
@@ -475,7 +506,7 @@ struct Walk {
                 uint16_t* Kn = smem + (stage ^ 1) * G::STAGE_ELEMS;
                 issue_tile<D>(Kbh, Vbh, next * BK, L, tid, Kn, Kn + G::KS_ELEMS);
             }
-            if (wave_active) tile<KIND>(acc, q, Ks, Vs, t * BK);
+            if (wave_active) tile<KIND, FINE>(acc, q, Ks, Vs, t * BK);
             wait_vm_all();
             __syncthreads();
             stage ^= 1;
@@ -526,17 +557,17 @@ struct Walk {
         }
     }
 
-    template <int KIND>
+    template <int KIND, bool FINE>
     __device__ __forceinline__ void tile(Acc<D, QB>& acc, const QFrag<D, QB>& q, const uint16_t* Ks, const uint16_t* Vs,
                                          int k0) {
         if constexpr (KIND == SEG_PLAIN) {
             Tile<QB> S;
             score_tile<D>(Ks, q, S, r, g);
-            accumulate<D, MASK_NONE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
+            accumulate<D, MASK_NONE, QB, FINE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
         } else if constexpr (KIND == SEG_KEYS) {
             Tile<QB> S;
             score_tile<D>(Ks, q, S, r, g);
-            accumulate<D, MASK_KEYS>(acc, S, Vs, r, g, qw0, k0, L, w, c);
+            accumulate<D, MASK_KEYS, QB, FINE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
         } else {
             // classify the tile against this wavefront's queries
             const bool ragged = k0 + BK > L;
@@ -546,11 +577,11 @@ struct Walk {
             Tile<QB> S;
             score_tile<D>(Ks, q, S, r, g);
             if (cls == TILE_BOUNDARY)
-                accumulate<D, KIND == SEG_BAND_IN ? MASK_BAND_IN : MASK_BAND_OUT>(acc, S, Vs, r, g, qw0, k0, L, w, c);
+                accumulate<D, KIND == SEG_BAND_IN ? MASK_BAND_IN : MASK_BAND_OUT, QB, FINE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
             else if (ragged)
-                accumulate<D, MASK_KEYS>(acc, S, Vs, r, g, qw0, k0, L, w, c);
+                accumulate<D, MASK_KEYS, QB, FINE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
             else
-                accumulate<D, MASK_NONE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
+                accumulate<D, MASK_NONE, QB, FINE>(acc, S, Vs, r, g, qw0, k0, L, w, c);
         }
     }
 };
@@ -608,7 +639,11 @@ __device__ __forceinline__ void refresh_split(const Params& p, uint16_t* smem, W
 template <int D, int KMODE, int QB>
 __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     using G = Geo<D>;
-    constexpr int MODE = KMODE == MODE_ASC ? MODE_FULL : (KMODE == MODE_REFRESH_SPLIT ? MODE_REFRESH : KMODE);
+    constexpr int MODE = KMODE == MODE_ASC             ? MODE_FULL
+                         : KMODE == MODE_REFRESH_SPLIT ? MODE_REFRESH
+                         : KMODE == MODE_WINDOW_FINE   ? MODE_WINDOW
+                                                       : KMODE;
+    constexpr bool FINE = KMODE == MODE_WINDOW_FINE;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -730,9 +765,9 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
         wk.template run<SEG_PLAIN>(acc, q, s0[0], s1[0], nxt[1]);
         wk.template run<SEG_KEYS>(acc, q, s0[1], s1[1], nxt[2]);
     } else {
-        wk.template run<SEG_BAND_IN>(acc, q, s0[0], s1[0], nxt[1]);
-        wk.template run<SEG_PLAIN>(acc, q, s0[1], s1[1], nxt[2]);
-        wk.template run<SEG_BAND_IN>(acc, q, s0[2], s1[2], nxt[3]);
+        wk.template run<SEG_BAND_IN, FINE>(acc, q, s0[0], s1[0], nxt[1]);
+        wk.template run<SEG_PLAIN, FINE>(acc, q, s0[1], s1[1], nxt[2]);
+        wk.template run<SEG_BAND_IN, FINE>(acc, q, s0[2], s1[2], nxt[3]);
     }
 
     if constexpr (MODE == MODE_REFRESH) {
@@ -897,7 +932,21 @@ hipError_t launch_refresh(const AttnLaunch& a, hipStream_t s) {
         default: return hipErrorInvalidValue;
     }
 }
-hipError_t launch_window(const AttnLaunch& a, hipStream_t s) { return launch_mode<MODE_WINDOW>(a, s); }
+// Narrow bands (at most 31 keys per query) apply each probability as a bf16
+// value plus its bf16 rounding residual: with so few keys per row the bf16
+// rounding of the weights does not average out, and alone it costs up to
+// 2^-8 max|v - o| per output.  Such bands always take 64-query workgroups.
+// A band covering every key keeps full attention's choice.
+hipError_t launch_window(const AttnLaunch& a, hipStream_t s) {
+    if (a.w <= FINE_MAX_HALF_WIDTH && a.w < a.L - 1) {
+        switch (a.d) {
+            case 64: return launch_attn<64, MODE_WINDOW_FINE, 1>(a, s);
+            case 72: return launch_attn<72, MODE_WINDOW_FINE, 1>(a, s);
+            default: return hipErrorInvalidValue;
+        }
+    }
+    return launch_mode<MODE_WINDOW>(a, s);
+}
 
 hipError_t launch_copy(const void* src, void* dst, size_t bytes, hipStream_t stream) {
     const size_t n16 = bytes / 16;

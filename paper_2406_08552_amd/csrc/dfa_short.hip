@@ -87,12 +87,22 @@ __device__ __forceinline__ float pair_acc(uint32_t w, float acc) {
 
 __device__ __forceinline__ u32x4 load16(const uint16_t* p) { return *(const u32x4*)p; }
 
+// The rounding residuals lo - bf16(lo) and hi - bf16(hi) of a pair packed by
+// pack_bf16x2 (exact in fp32), themselves packed to bf16.
+__device__ __forceinline__ uint32_t pack_residual(float lo, float hi, uint32_t packed) {
+    return pack_bf16x2(lo - __builtin_bit_cast(float, packed << 16), hi - __builtin_bit_cast(float, packed & 0xFFFF0000u));
+}
+
 // Probabilities of one query block (lane: query 16 qb + r, keys 16 kb + 4 g + i)
 // under the key set of BAND (all keys < L, or also |i - j| <= w), packed as
-// the PV B operand; psum gets the fp32 sum of the packed (rounded) values
-// over the lane's keys.
+// two PV B operands: the bf16 values, and `res`, their rounding residuals in
+// bf16.  A row has at most 32 keys here, too few to average the bf16
+// rounding of its weights (up to 2^-8 max|v - o| per output); the two
+// products together apply each weight to about 2^-16 relative.  psum gets the
+// fp32 sum of both packed operands over the lane's keys.
 template <int NB, bool BAND>
-__device__ __forceinline__ bf16x8 probs(const f32x4 (&s)[NB], int qi, int g, int L, int w, float c, float& psum) {
+__device__ __forceinline__ bf16x8 probs(const f32x4 (&s)[NB], int qi, int g, int L, int w, float c, float& psum,
+                                        bf16x8& res) {
     float v[NB][4];
     float mx = NEG_INF;
 #pragma unroll
@@ -109,7 +119,7 @@ __device__ __forceinline__ bf16x8 probs(const f32x4 (&s)[NB], int qi, int g, int
     mx = fmaxf(mx, __shfl_xor(mx, 32));
     // a query row beyond L may have no key in its band; its output is never stored
     const float negm = mx == NEG_INF ? 0.f : -mx * c;
-    uint32_t wd[4] = {0u, 0u, 0u, 0u};
+    uint32_t wd[4] = {0u, 0u, 0u, 0u}, rd[4] = {0u, 0u, 0u, 0u};
     psum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < NB; ++kb) {
@@ -118,8 +128,12 @@ __device__ __forceinline__ bf16x8 probs(const f32x4 (&s)[NB], int qi, int g, int
         for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(v[kb][i], c, negm));
         wd[2 * kb + 0] = pack_bf16x2(p[0], p[1]);
         wd[2 * kb + 1] = pack_bf16x2(p[2], p[3]);
+        rd[2 * kb + 0] = pack_residual(p[0], p[1], wd[2 * kb + 0]);
+        rd[2 * kb + 1] = pack_residual(p[2], p[3], wd[2 * kb + 1]);
         psum = pair_acc(wd[2 * kb + 1], pair_acc(wd[2 * kb], psum));
+        psum = pair_acc(rd[2 * kb + 1], pair_acc(rd[2 * kb], psum));
     }
+    res = __builtin_bit_cast(bf16x8, u32x4{rd[0], rd[1], rd[2], rd[3]});
     return __builtin_bit_cast(bf16x8, u32x4{wd[0], wd[1], wd[2], wd[3]});
 }
 
@@ -258,11 +272,14 @@ short_attn_kernel(SParams p) {
 #pragma unroll
         for (int set = 0; set < NSET; ++set) {
             float psum;
-            const bf16x8 pb = (MODE == MODE_WINDOW || set == 1) ? probs<NB, true>(S[qb], qi, g, L, w, c, psum)
-                                                                 : probs<NB, false>(S[qb], qi, g, L, w, c, psum);
+            bf16x8 pr;
+            const bf16x8 pb = (MODE == MODE_WINDOW || set == 1) ? probs<NB, true>(S[qb], qi, g, L, w, c, psum, pr)
+                                                                 : probs<NB, false>(S[qb], qi, g, L, w, c, psum, pr);
 #pragma unroll
-            for (int mb = 0; mb < G::NDB; ++mb)
+            for (int mb = 0; mb < G::NDB; ++mb) {
                 o[set][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[mb], pb, f32x4{0.f, 0.f, 0.f, 0.f}, 0, 0, 0);
+                o[set][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[mb], pr, o[set][mb], 0, 0, 0);
+            }
             float l;
             if constexpr (G::ONES) {
                 // row sum: output dim D of the query, held by lane 16 (D % 16 / 4) + r
