@@ -28,6 +28,12 @@
  *            |i - j| <= w over the flattened token index (a band along the
  *            diagonal of the attention matrix, Sec. 3.2), truncated at 0 and
  *            L-1.  w is the HALF-width; w >= L-1 covers every key.
+ *   Numerics Scores and softmax statistics are fp32; the probabilities enter
+ *            the PV product as bf16 and every accumulation is fp32.  Rows of
+ *            at most 32 keys (windows with w <= 15, and every sequence of at
+ *            most 32 tokens) add the bf16 rounding residual of each
+ *            probability as a second PV operand: with so few keys the
+ *            rounding of the weights does not average out.
  *   CFG      A classifier-free-guidance batch holds B = 2P entries: entries
  *            0..P-1 are the conditional evaluations and entry b + P is the
  *            unconditional partner of entry b (Sec. 3.4).
