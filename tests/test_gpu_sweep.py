@@ -93,3 +93,56 @@ def test_sweep_draws_are_fixed():
     assert any(c[2] <= 32 for c in a) and any(c[2] > 1000 for c in a)
     assert any(c[4] >= c[2] - 1 for c in a) and any(c[4] <= 1 for c in a)
     assert np.mean([c[3] == 72 for c in a]) > 0.2
+
+
+N_LARGE = 24
+
+
+def draw_large_cases(seed: int, n: int):
+    """Launches of more than 256 128-query workgroups (the two-block kernels):
+    L from 300 to 9000 tokens and B*H to match, half-widths from 0 to beyond L."""
+    rng = random.Random(seed)
+    cases = []
+    for _ in range(n):
+        d = rng.choice([64, 72])
+        L = int(round(10 ** rng.uniform(np.log10(300), np.log10(9000))))
+        bh_min = 257 * 128 // L + 1
+        B = rng.choice([2, 4, 8])
+        H = max(1, -(-bh_min // B)) + rng.randint(0, 3)
+        w = rng.choice([0, 3, 16, rng.randint(17, 200), L // 8, rng.randint(0, L), max(0, L - 2), L - 1, 2 ** 31 - 1])
+        cases.append((B, H, L, d, w))
+    return cases
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("case,B,H,L,d,w", [(i, *c) for i, c in enumerate(draw_large_cases(4242, N_LARGE))])
+def test_random_large_launch(case, B, H, L, d, w):
+    """Checked on 40 sampled query rows of every (batch, head): both sequence
+    ends, the rows around the first query-block boundaries, and a seeded sample."""
+    dev = torch.device("cuda")
+    shape = (B, H, L, d)
+    say(f"large sweep case {case}: B={B} H={H} L={L} d={d} w={w}")
+    q, k, v = rand_qkv(shape, 7000 + case)
+    Rres = rand_qkv(shape, 7100 + case)[0].float() * 0.1
+    gq, gk, gv, gr = (t.to(dev) for t in (q, k, v, Rres))
+    O1, O2, O3 = (torch.empty(shape, dtype=torch.bfloat16, device=dev) for _ in range(3))
+    R2 = torch.empty(shape, dtype=torch.float32, device=dev)
+    dfa.dfa_attn_full(gq, gk, gv, O1, w)
+    dfa.dfa_attn_full_and_residual(gq, gk, gv, O2, R2, w)
+    dfa.dfa_attn_window_plus_residual(gq, gk, gv, O3, gr, w)
+    torch.cuda.synchronize()
+    fixed = [0, 1, 63, 64, 127, 128, 129, L // 2, L - 129, L - 128, L - 65, L - 64, L - 2, L - 1]
+    rows = np.unique(np.concatenate([fixed, np.random.default_rng(7200 + case).integers(0, L, 26)]))
+    Qd, Kd, Vd = f64(q), f64(k), f64(v)
+    Of = orc.attention_rows(Qd, Kd, Vd, rows, None)
+    Wd = orc.attention_rows(Qd, Kd, Vd, rows, w)
+    check("full", O1, Of, rows)
+    check("refresh O", O2, Of, rows)
+    check("refresh R", R2, Of - Wd, rows)
+    check("window + R", O3, Wd + f64(Rres)[:, :, rows], rows)
+
+
+def test_large_draws_take_two_block_kernels():
+    """Every large case launches more than 256 128-query workgroups."""
+    for B, H, L, d, w in draw_large_cases(4242, N_LARGE):
+        assert B * H * -(-L // 128) > 256 and 300 <= L <= 9000
