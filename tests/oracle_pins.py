@@ -487,10 +487,72 @@ def pin_search():
         _replay_check(Xs, layers, plan, delta, w)
 
 
+# P16 -- sampled-row evaluation (the reference of every long-sequence parity
+# check): attention rows are independent (Eq. (1)-(2) per query row), so the
+# output of any set of query rows, taken in row blocks, must equal those rows
+# of a whole-sequence evaluation by an independent library, and the sampled
+# plan step must equal the same rows of the whole plan step through every
+# plan code (the caches of Sec. 3.2-3.4 carried per row).
+def _sdpa_rows(Q, K, V, rows, w):
+    tq, tk, tv = (torch.from_numpy(np.ascontiguousarray(x)) for x in (Q, K, V))
+    mask = None
+    if w is not None:
+        i = torch.arange(Q.shape[2])
+        mask = (i[:, None] - i[None, :]).abs() <= w
+    return torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, attn_mask=mask).numpy()[:, :, rows]
+
+
+def _sampled_rows(L, n, seed, fixed=()):
+    rng = np.random.Generator(np.random.PCG64(seed))
+    extra = rng.choice(L, size=n, replace=False)
+    return np.unique(np.concatenate([np.asarray(fixed, dtype=np.int64), extra]))
+
+
+def pin_sampled_rows():
+    # several row blocks of a non-contiguous row set (the block size lowered)
+    B, H, L, d = 1, 2, 70, 16
+    Q, K, V = (_rand((B, H, L, d), s + 160) for s in (1, 2, 3))
+    rows = np.array([0, 2, 3, 7, 11, 12, 30, 31, 44, 50, 68, 69])
+    saved = O._ROW_BLOCK
+    try:
+        O._ROW_BLOCK = 5
+        for w in (None, 0, 3, 9, 69):
+            got = O.attention_rows(Q, K, V, rows, w)
+            assert np.max(np.abs(got - _sdpa_rows(Q, K, V, rows, w))) <= 1e-12, w
+    finally:
+        O._ROW_BLOCK = saved
+    # at the real block size: rows on both sides of each block boundary
+    B, H, L, d, w = 1, 1, 1300, 8, 162
+    Q, K, V = (_rand((B, H, L, d), s + 170, 1.5) for s in (1, 2, 3))
+    rows = _sampled_rows(L, 20, 171, (0, 1, 161, 162, 163, 861, 862, 1023, 1024, 1025, 1137, 1138, 1299))
+    for ww in (None, w):
+        assert np.max(np.abs(O.attention_rows(Q, K, V, rows, ww) - _sdpa_rows(Q, K, V, rows, ww))) <= 1e-12
+    full = O.attention_rows(Q, K, V, np.arange(L), w)
+    assert np.max(np.abs(full[:, :, rows] - _sdpa_rows(Q, K, V, rows, w))) <= 1e-12
+    # the sampled plan step against the whole plan step, every code, drifting inputs
+    B, H = 2, 1
+    codes = [O.WARS_REFRESH, O.WARS_REUSE, O.WARS_ASC_REUSE, O.AST_REUSE, O.WARS_ASC_REFRESH, O.WARS_ASC_REUSE,
+             O.ASC_REUSE, O.FULL, O.AST_REUSE, O.WARS_REFRESH, O.WARS_REUSE]
+    X = [_rand((B, H, L, d), s + 180, 1.5) for s in (1, 2, 3)]
+    whole, part = O.LayerCache(), O.LayerCache()
+    for t, c in enumerate(codes):
+        X = [x + 0.05 * _rand(x.shape, 190 + 3 * t + s) for s, x in enumerate(X)]
+        ref = O.plan_step(c, *X, whole, w)
+        got = O.plan_step_rows(c, *X, rows, part, w)
+        assert got.shape == (B, H, len(rows), d)
+        assert np.max(np.abs(got - ref[:, :, rows])) <= 1e-12, (t, O.CODE_NAMES[c])
+        assert np.max(np.abs(part.R - whole.R[:, :, rows])) <= 1e-12, (t, O.CODE_NAMES[c])
+    # the sampled step reads its residual: a reuse at unchanged inputs rebuilds the refresh
+    part = O.LayerCache()
+    Or = O.plan_step_rows(O.WARS_REFRESH, *X, rows, part, w)
+    assert np.max(np.abs(O.plan_step_rows(O.WARS_REUSE, *X, rows, part, w) - Or)) <= 1e-12
+    assert np.max(np.abs(part.R)) > 1e-3
+
+
 ALL_PINS = {
     "P1": pin_brute_force, "P2": pin_torch_sdpa, "P3": pin_wide_band, "P4": pin_zero_band,
     "P5": pin_zero_query, "P6": pin_constant_values, "P7": pin_probabilities,
     "P8": pin_refresh_reuse_algebra, "P9": pin_sharing, "P10": pin_permutation,
     "P11": pin_table2, "P12": pin_plan, "P13": pin_wars_asc, "P14": pin_module,
-    "P15": pin_search,
+    "P15": pin_search, "P16": pin_sampled_rows,
 }

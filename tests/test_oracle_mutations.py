@@ -11,7 +11,8 @@ from oracle import dfa_oracle as O
 from tests import oracle_pins as pins
 
 # cheap pins first: a mutation stops at the first pin that catches it
-ORDER = ["P4", "P3", "P6", "P7", "P5", "P8", "P9", "P10", "P12", "P13", "P14", "P15", "P2", "P1", "P11"]
+ORDER = ["P4", "P3", "P6", "P7", "P5", "P8", "P9", "P10", "P12", "P13", "P14", "P15", "P2", "P1", "P16",
+         "P11"]
 
 
 def _probs_factory(scale_fn=None, transpose=False, axis=-1):
@@ -279,6 +280,33 @@ def _plan_ast_at_start(seed, n_layers, n_steps, refresh_every, B):
     return code, r_src, o_src
 
 
+def _rows_block_local(Q, K, V, rows, w=None):
+    # the band built from indices within the row block instead of token indices
+    Q, K, V = (np.asarray(x, dtype=np.float64) for x in (Q, K, V))
+    rows = np.asarray(rows, dtype=np.int64)
+    B, H, L, d = Q.shape
+    out = np.empty((B, H, len(rows), d))
+    for b in range(B):
+        for h in range(H):
+            for r0 in range(0, len(rows), O._ROW_BLOCK):
+                rr = rows[r0:r0 + O._ROW_BLOCK]
+                P = O.attention_probs(Q[b, h, rr], K[b, h], w, np.arange(len(rr)))
+                out[b, h, r0:r0 + len(rr)] = P @ V[b, h]
+    return out
+
+
+_plan_step_rows = O.plan_step_rows
+
+
+def _rows_reuse_on_full(code, Q, K, V, rows, cache, w):
+    # the sampled reuse step evaluated on full attention instead of the window
+    if code == O.WARS_REUSE:
+        Ofull = O.attention_rows(Q, K, V, rows, None) + O._residual_for(code, cache, np.shape(Q)[0])
+        cache.O_cache = Ofull
+        return Ofull
+    return _plan_step_rows(code, Q, K, V, rows, cache, w)
+
+
 MUTATIONS = {
     "scale_1_over_d": ("attention_probs", _probs_factory(scale_fn=lambda d: 1.0 / d)),
     "scale_missing": ("attention_probs", _probs_factory(scale_fn=lambda d: 1.0)),
@@ -310,6 +338,8 @@ MUTATIONS = {
     "splitmix_shift_typo": ("SplitMix64", _SplitMixTypo),
     "refresh_age_off_by_one": ("plan_make", _plan_age_off_by_one),
     "ast_at_first_step": ("plan_make", _plan_ast_at_start),
+    "rows_band_block_local": ("attention_rows", _rows_block_local),
+    "rows_reuse_on_full": ("plan_step_rows", _rows_reuse_on_full),
 }
 
 
