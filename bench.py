@@ -86,6 +86,109 @@ def timed(torch, stream, fn, reps):
     return s0.elapsed_time(s1) / reps
 
 
+def interleaved(torch, stream, fns, reps, rounds=5):
+    """Median ms per call of every fn in ``fns`` (name -> callable), timed in
+    rounds that run each fn ``reps`` times in turn, so that all of them see the
+    same clock and cache conditions (HIP events on the launch stream)."""
+    import statistics
+    for fn in fns.values():
+        fn()
+    torch.cuda.synchronize()
+    ms = {name: [] for name in fns}
+    for _ in range(rounds):
+        for name, fn in fns.items():
+            s0 = torch.cuda.Event(enable_timing=True)
+            s1 = torch.cuda.Event(enable_timing=True)
+            s0.record(stream)
+            for _ in range(reps):
+                fn()
+            s1.record(stream)
+            torch.cuda.synchronize()
+            ms[name].append(s0.elapsed_time(s1) / reps)
+    return {name: statistics.median(v) for name, v in ms.items()}
+
+
+class ClockSampler:
+    """Samples the GPU shader clock from the driver's sysfs table (the level
+    marked current in pp_dpm_sclk) on a host thread while a workload runs.
+    Best effort: reports None where the file is not readable."""
+
+    def __init__(self, period_s=0.02):
+        import glob
+        import threading
+        self.paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.samples, self.period = [], period_s
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        for path in self.paths:
+            try:
+                with open(path) as f:
+                    for line in f:
+                        if line.rstrip().endswith("*"):
+                            m = re.search(r"(\d+)\s*[Mm]hz", line)
+                            if m:
+                                return int(m.group(1))
+            except OSError:
+                continue
+        return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            v = self._read()
+            if v is not None:
+                self.samples.append(v)
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self.paths:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._thread.is_alive():
+            self._thread.join()
+
+    def summary(self):
+        if not self.samples:
+            return None
+        v = sorted(self.samples)
+        return {"median_mhz": v[len(v) // 2], "min_mhz": v[0], "max_mhz": v[-1], "samples": len(v),
+                "source": "pp_dpm_sclk current level, sampled during the full-attention-only pass"}
+
+
+def environment(torch):
+    """Software and hardware the numbers were measured on."""
+    env = {"torch": torch.__version__, "hip_runtime": getattr(torch.version, "hip", None)}
+    try:
+        with open("/opt/rocm/.info/version") as f:
+            env["rocm"] = f.read().strip()
+    except OSError:
+        env["rocm"] = None
+    try:
+        props = torch.cuda.get_device_properties(0)
+        env["gpu"] = props.name
+        env["gcn_arch"] = getattr(props, "gcnArchName", None)
+        env["compute_units"] = props.multi_processor_count
+        env["hbm_gib"] = round(props.total_memory / 2 ** 30, 1)
+    except Exception:  # pragma: no cover
+        env["gpu"] = None
+    return env
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def video_bench(args, dfa, inputs, torch, dev, stream):
     """Attention kernels at the Open-Sora V1.1 240p 16-frame shapes: spatial
     attention within frames (32 sequences of 405 tokens per head) and
@@ -197,9 +300,9 @@ def module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres):
         dfa.dfa_module_step(c, X[l], Wqkv, bqkv, Wo, bo, Q, K, V, O, R[l], Y[l], Y[l], w, H, stream)
 
     step(dfa.WARS_REFRESH, 0)
-    per = {}
-    for c in (dfa.FULL, dfa.WARS_REFRESH, dfa.WARS_REUSE, dfa.ASC_REUSE, dfa.WARS_ASC_REUSE, dfa.AST_REUSE):
-        per[dfa.CODE_NAMES[c].lower()] = round(timed(torch, stream, lambda c=c: step(c, 0), reps), 4)
+    codes = (dfa.FULL, dfa.WARS_REFRESH, dfa.WARS_REUSE, dfa.ASC_REUSE, dfa.WARS_ASC_REUSE, dfa.AST_REUSE)
+    per = {k: round(v, 4) for k, v in interleaved(
+        torch, stream, {dfa.CODE_NAMES[c].lower(): (lambda c=c: step(c, 0)) for c in codes}, reps).items()}
 
     def module_pass(codes):
         for t in range(NS):
@@ -231,7 +334,8 @@ def module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres):
         "out_proj": {"ms": round(ms_out, 4), "tflops": round(out_flops / (ms_out * 1e-3) / 1e12, 1)},
         "ms_per_module_step": per,
         # module time of each strategy's compressed step relative to the
-        # uncompressed module (Table 2's latency rows are module-level)
+        # uncompressed module (Table 2's latency rows are module-level), from
+        # the interleaved repetitions above
         "latency_fraction_vs_full": {
             name: round(per[key] / per["full"], 4)
             for name, key in (("asc", "asc_reuse"), ("wars", "wars_reuse"), ("wars_asc", "wars_asc_reuse"),
@@ -259,20 +363,26 @@ def parse():
 
 
 def cpu_baseline(cfg, target_s: float):
-    """The fp64 oracle (as it is) on a bounded sample of one FULL layer-step:
-    every (batch, head) for a seeded sample of query rows, sized to about
-    target_s seconds of host work, scaled to TFLOP/s."""
+    """The fp64 oracle (as it is) on a bounded sample of one layer-step: every
+    (batch, head) for a seeded sample of query rows, sized so that full
+    attention takes about target_s / 4 seconds of host work; `value` is that
+    full-attention rate in TFLOP/s.  Then one layer-step per plan code on the
+    same rows (refresh, reuse, ASC, full, AST, through the oracle's sampled
+    plan step) with its time in ms."""
     import numpy as np
 
     from oracle import dfa_oracle as orc
     from paper_2406_08552_amd import inputs
+    blas = None
     try:
         from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"),
-                      default=1)
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        threads = max((i.get("num_threads", 1) for i in info), default=1)
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')} ({info[0].get('threading_layer')})"
     except Exception:  # pragma: no cover
         threads = len(os.sched_getaffinity(0))
-    B, H, L, d = cfg.B, cfg.H, cfg.L, cfg.d
+    B, H, L, d, w = cfg.B, cfg.H, cfg.L, cfg.d, cfg.w
     rng = np.random.Generator(np.random.PCG64(inputs.SEED_BASE + 7))
     # one layer's Q/K/V rounded to bf16, as the GPU sees them
     import torch
@@ -288,9 +398,18 @@ def cpu_baseline(cfg, target_s: float):
         if elapsed >= target_s / 4 or n_rows >= L:
             break
         n_rows = min(L, n_rows * 4 if elapsed < target_s / 16 else n_rows * 2)
+    per_code = {}
+    cache = orc.LayerCache()
+    for c in (orc.WARS_REFRESH, orc.WARS_REUSE, orc.ASC_REUSE, orc.FULL, orc.AST_REUSE):
+        t0 = time.perf_counter()
+        orc.plan_step_rows(c, Q, K, V, rows, cache, w)
+        per_code[orc.CODE_NAMES[c].lower()] = round((time.perf_counter() - t0) * 1e3, 2)
     return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"full attention of {len(rows)} seeded query rows x all {B * H} (batch, head) pairs of one "
-                      f"L={L} d={d} layer-step, fp64 numpy, {elapsed:.2f} s"}
+                      f"L={L} d={d} layer-step, fp64 numpy, {elapsed:.2f} s",
+            "cpu_model": cpu_model(), "blas": blas,
+            "oracle_ms_per_layer_step_on_sample": per_code,
+            "rows_per_head": len(rows)}
 
 
 def main():
@@ -372,10 +491,11 @@ def main():
     f0 = time.perf_counter()
     fs = torch.cuda.Event(enable_timing=True)
     fe = torch.cuda.Event(enable_timing=True)
-    fs.record(stream)
-    plan_pass(full_codes)
-    fe.record(stream)
-    torch.cuda.synchronize()
+    with ClockSampler() as clock:
+        fs.record(stream)
+        plan_pass(full_codes)
+        fe.record(stream)
+        torch.cuda.synchronize()
     full_only_ms = max(fs.elapsed_time(fe), (time.perf_counter() - f0) * 1e3)
 
     # per-kernel times at the same shape (each entry point on its own)
@@ -400,17 +520,9 @@ def main():
     }
     tensor_bytes = B * H * L * d * 2
     kres = {}
+    kms = interleaved(torch, stream, {name: fn for name, (fn, _, _) in kernels.items()}, args.kernel_reps)
     for name, (fn, fl, ntens) in kernels.items():
-        fn()
-        torch.cuda.synchronize()
-        s0 = torch.cuda.Event(enable_timing=True)
-        s1 = torch.cuda.Event(enable_timing=True)
-        s0.record(stream)
-        for _ in range(args.kernel_reps):
-            fn()
-        s1.record(stream)
-        torch.cuda.synchronize()
-        ms = s0.elapsed_time(s1) / args.kernel_reps
+        ms = kms[name]
         tflops = fl / (ms * 1e-3) / 1e12 if fl else 0.0
         gbs = ntens * tensor_bytes / (ms * 1e-3) / 1e9
         kres[name] = {"ms": round(ms, 4), "tflops": round(tflops, 1), "gbs": round(gbs, 1),
@@ -420,8 +532,19 @@ def main():
     module = module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres)
     video = video_bench(args, dfa, inputs, torch, dev, stream)
 
-    full_ms = sum(per_code.get(0, [])) / max(1, len(per_code.get(0, [])))
+    def plan_mean(c):
+        v = per_code.get(c, [])
+        return sum(v) / len(v) if v else None
+
+    full_ms = plan_mean(0) or 0.0
     full_flops = code_flops(0, B, H, L, d, w)
+    # ratios to full attention under one timing condition: the timed plan's
+    # own per-entry events where the plan runs the code, otherwise the
+    # interleaved per-kernel repetitions (both numbers of a ratio from one source)
+    in_plan = {"asc": 4, "wars": 2, "wars_refresh": 1}
+    frac = {name: round(plan_mean(c) / full_ms, 4) for name, c in in_plan.items() if plan_mean(c) and full_ms}
+    frac.update({name: round(kres[key]["ms"] / kres["full"]["ms"], 4)
+                 for name, key in (("wars_asc", "wars_asc_reuse"), ("ast", "ast_copy"))})
     achieved = full_flops / (full_ms * 1e-3) / 1e12 if full_ms > 0 else 0.0
     plan_layer_steps = NL * NS
     out = {
@@ -449,16 +572,22 @@ def main():
         "plan_code_counts": {dfa.CODE_NAMES[c].lower(): int((code == c).sum()) for c in range(5)},
         # kernel time of each strategy's compressed step relative to full
         # attention at the same shape (the latency rows of Table 2)
-        "latency_fraction_vs_full": {
+        "latency_fraction_vs_full": frac,
+        "latency_fraction_timing": "asc, wars (reuse) and wars_refresh: mean per-entry HIP events of the timed plan "
+                                   "passes; wars_asc (reuse) and ast (copy): interleaved per-kernel repetitions",
+        "latency_fraction_vs_full_interleaved": {
             name: round(kres[key]["ms"] / kres["full"]["ms"], 4)
-            for name, key in (("asc", "asc"), ("wars", "wars_reuse"), ("wars_asc", "wars_asc_reuse"),
-                              ("ast", "ast_copy"))},
+            for name, key in (("asc", "asc"), ("wars", "wars_reuse"), ("wars_refresh", "wars_refresh"),
+                              ("wars_asc", "wars_asc_reuse"), ("ast", "ast_copy"))},
         "full_equiv_tflops": round(plan_layer_steps * full_flops / (ms_per_step * 1e-3) / 1e12, 1),
         "kernels": kres,
         "module": module,
         "video": video,
-        "reuse_speedup_vs_full": round(kres["full"]["ms"] / kres["wars_reuse"]["ms"], 3),
+        # full / reuse time, both from the timed plan's per-entry events
+        "reuse_speedup_vs_full": round(full_ms / plan_mean(2), 3) if plan_mean(2) else None,
+        "reuse_speedup_vs_full_interleaved": round(kres["full"]["ms"] / kres["wars_reuse"]["ms"], 3),
         "reuse_ideal_speedup": round(L * L / n_band(L, w), 3),
+        "environment": {**environment(torch), "sclk": clock.summary()},
         "roofline": {"kernel": "attn_kernel<72, 0, 2> (full attention, 128-query workgroups: dfa_attn_full / FULL plan entries)", "bound": "mfma",
                      "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4),

@@ -52,7 +52,8 @@
 //   moves by up to 2^-8 max|v - o| on top of its own bf16 rounding.  Bands of
 //   at most 31 keys per query therefore apply each probability twice: as its
 //   bf16 value and as the bf16 rounding of its residual p - bf16(p), in two PV
-//   products, so each weight is applied to about 2^-16 relative.
+//   products, so each weight is applied to about 2^-16 relative.  The refresh
+//   does the same in its in-band phase, which forms W.
 //
 // Tile walk and band handling
 //   The key tiles a workgroup visits are split into segments so that the hot
@@ -97,12 +98,18 @@ constexpr float RESCALE_THRESH = 8.0f;    // lazy rescale margin (log2 units)
 constexpr int FINE_MAX_HALF_WIDTH = 15;   // window half-widths applied with split probabilities
 constexpr float NEG_INF = -__builtin_inff();
 
-enum { MODE_FULL = 0, MODE_REFRESH = 1, MODE_WINDOW = 2, MODE_ASC = 3, MODE_REFRESH_SPLIT = 4, MODE_WINDOW_FINE = 5 };
+enum {
+    MODE_FULL = 0, MODE_REFRESH = 1, MODE_WINDOW = 2, MODE_ASC = 3, MODE_REFRESH_SPLIT = 4, MODE_WINDOW_FINE = 5,
+    MODE_REFRESH_FINE = 6
+};
 // MODE_ASC computes exactly what MODE_FULL computes (on the conditional half of
 // the batch, storing every tile to both halves); it is a separate
 // instantiation only so that profiles report it apart from full attention.
 // MODE_REFRESH_SPLIT computes what MODE_REFRESH computes, in one pass with two
 // accumulators instead of two phases with one (short sequences).
+// MODE_REFRESH_FINE is the two-phase refresh for bands of at most 31 keys: its
+// in-band phase (the window attention W) applies split probabilities, like
+// MODE_WINDOW_FINE; the out-of-band phase, over all other keys, plain ones.
 enum { MASK_NONE = 0, MASK_KEYS = 1, MASK_BAND_IN = 2, MASK_BAND_OUT = 3 };
 enum { TILE_INSIDE = 0, TILE_OUTSIDE = 1, TILE_BOUNDARY = 2 };
 // segment kinds of the tile walk
@@ -641,9 +648,11 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     using G = Geo<D>;
     constexpr int MODE = KMODE == MODE_ASC             ? MODE_FULL
                          : KMODE == MODE_REFRESH_SPLIT ? MODE_REFRESH
+                         : KMODE == MODE_REFRESH_FINE  ? MODE_REFRESH
                          : KMODE == MODE_WINDOW_FINE   ? MODE_WINDOW
                                                        : KMODE;
-    constexpr bool FINE = KMODE == MODE_WINDOW_FINE;
+    // split probabilities in the in-band segments (the window attention)
+    constexpr bool FINE = KMODE == MODE_WINDOW_FINE || KMODE == MODE_REFRESH_FINE;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -924,7 +933,17 @@ hipError_t launch_asc(const AttnLaunch& a, hipStream_t s) { return launch_mode<M
 // Refresh: the one-pass two-accumulator form up to L = 512 (8 key tiles, where
 // band-edge tiles are most of the walk), the two-phase form beyond (measured:
 // L = 256 -16%, 405 -6%, 1024 +3% for the one-pass form).
+// Bands of at most 31 keys take the two-phase form with split probabilities
+// in its in-band phase (64-query workgroups), so that W, and with it R and
+// every reuse that adds R, carries no unaveraged bf16 rounding of its weights.
 hipError_t launch_refresh(const AttnLaunch& a, hipStream_t s) {
+    if (a.w <= FINE_MAX_HALF_WIDTH && a.w < a.L - 1) {
+        switch (a.d) {
+            case 64: return launch_attn<64, MODE_REFRESH_FINE, 1>(a, s);
+            case 72: return launch_attn<72, MODE_REFRESH_FINE, 1>(a, s);
+            default: return hipErrorInvalidValue;
+        }
+    }
     if (a.L > 512) return launch_mode<MODE_REFRESH>(a, s);
     switch (a.d) {
         case 64: return launch_attn<64, MODE_REFRESH_SPLIT, 1>(a, s);

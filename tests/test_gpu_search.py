@@ -2,15 +2,18 @@
 against the fp64 oracle, through the C ABI.
 
 MRAE: relative tolerance 1e-5 (each lane sums in fp32, partial sums in fp64).
-Plan search: the plan is a sequence of integer decisions, each taken by
-comparing a loss with a threshold, and the library computes its losses on
-bf16 activations while the oracle computes them in fp64.  The test therefore
-compares against the oracle run with the library's storage precision (Q, K,
-V, O and the hidden states rounded to bf16 where the library stores them),
-and first checks that the case is well posed: the oracle's plan must not
-change when delta moves by 3% either way, so no decision sits within 3% of
-its threshold.  Then the GPU plan must equal the oracle plan exactly, and the
-accepted losses must agree to 5% (relative) or n_layers * 2^-8 (absolute).
+Plan search: the expected plan is the fp64 oracle's Alg. 1 with the loss of
+the appendix, as the paper defines it (no storage rounding anywhere).  The plan
+is a sequence of integer decisions, each taken by comparing a loss with a
+threshold, and the library computes its losses on bf16 activations; so each
+case must first be well posed: the fp64 plan must not change when delta moves
+by 3% either way, and the same oracle with Q, K, V, O and the hidden states
+rounded to bf16 where the library stores them must give the same plan at all
+three deltas (so the library's storage precision cannot move a decision).
+Then the GPU plan must equal the fp64 plan exactly, and the accepted losses
+must agree with the fp64 losses to 5% (relative) or n_layers * 2^-8
+(absolute), plus the measured effect of bf16 storage on each loss (the
+storage-rounded oracle's loss minus the fp64 one).
 The absolute part: a compressed path may use another kernel than the
 reference path (ASC's conditional half runs the full-attention kernel, the
 uncompressed reference the refresh kernel), and their bf16 outputs can differ
@@ -90,21 +93,26 @@ def test_search_degenerate_cases():
     assert np.all(loss[1:] == 0.0), "AST of an unchanged input must reproduce the reference exactly"
 
 
-@pytest.mark.parametrize("drift,w,delta", [(0.08, 48, 0.09), (0.01, 16, 0.05), (0.05, 40, 0.2)])
+# the fp64 plans of these cases hold refresh, reuse and ASC; refresh, reuse,
+# AST and ASC; ASC and AST
+@pytest.mark.parametrize("drift,w,delta", [(0.08, 48, 0.09), (0.03, 24, 0.07), (0.05, 40, 0.2)])
 def test_search_vs_oracle(drift, w, delta):
     dev = torch.device("cuda")
     B, L, H, d, n, T = 2, 64, 2, 64, 3, 5
     Xs, Xg, lg, lo = _surrogate(dev, B, L, H, d, n, T, drift)
     Xd = [f64(x) for x in Xs]
-    ref, ref_loss = orc.plan_search(Xd, lo, delta, w, store=to_bf16_f64)
+    ref, ref_loss = orc.plan_search(Xd, lo, delta, w)
+    stored, stored_loss = orc.plan_search(Xd, lo, delta, w, store=to_bf16_f64)
+    assert np.array_equal(stored, ref), "ill-posed case: bf16 storage moves a decision"
     for scale in (0.97, 1.03):
-        other, _ = orc.plan_search(Xd, lo, delta * scale, w, store=to_bf16_f64)
-        assert np.array_equal(other, ref), "ill-posed case: a decision lies within 3% of its threshold"
+        for hook in (None, to_bf16_f64):
+            other, _ = orc.plan_search(Xd, lo, delta * scale, w, store=hook)
+            assert np.array_equal(other, ref), "ill-posed case: a decision lies within 3% of its threshold"
     say(f"search drift={drift} w={w} delta={delta}")
     plan, loss = _search_gpu(Xg, lg, delta, w, H)
     say(f"plan {plan.tolist()} oracle {ref.tolist()}")
     assert np.array_equal(plan, ref), (plan.tolist(), ref.tolist())
     both = ~np.isnan(ref_loss)
     assert np.array_equal(both, ~np.isnan(loss))
-    assert np.all(np.abs(loss[both] - ref_loss[both]) <= np.maximum(0.05 * ref_loss[both], n * 2.0 ** -8)), \
-        (loss.tolist(), ref_loss.tolist())
+    bar = np.maximum(0.05 * ref_loss[both], n * 2.0 ** -8) + np.abs(stored_loss[both] - ref_loss[both])
+    assert np.all(np.abs(loss[both] - ref_loss[both]) <= bar), (loss.tolist(), ref_loss.tolist())
