@@ -198,6 +198,23 @@ dfa_status dfa_module_step(int code, const void* X, const void* Wqkv, const void
 #define DFA_MRAE_WORKSPACE_BYTES 8192
 dfa_status dfa_mrae(const void* A, const void* B, size_t n, void* workspace, double* result, hipStream_t stream);
 
+/* dfa_mrae without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): same arguments otherwise, same kernels and grid, so
+ * the same result bit for bit.  It calls no hipMalloc, hipFree or other
+ * allocating routine.  Its per-workgroup partial sums live in a fixed device
+ * array of the library, 8 KiB (1024 fp64 values) per device, held from the
+ * first call on a device until the process ends; its address is looked up on
+ * that first call, with the calling thread's current device (the device of
+ * `stream`).  The grid of the reduction is capped at 1024 workgroups, so every
+ * n up to DFA_MRAE_NOALLOC_MAX_ELEMS fits; a larger n returns
+ * DFA_ERR_INVALID_ARG.  Every call on a device shares that device's array and
+ * leaves its partial sums there (each call writes every partial sum it reads,
+ * so nothing needs clearing); calls that overlap in time on one device, e.g.
+ * on two streams, race on it and must be serialised by the caller. */
+#define DFA_MRAE_NOALLOC_MAX_ELEMS (1ULL << 40)
+dfa_status dfa_mrae_noalloc(const void* A, const void* B, size_t n, double* result, hipStream_t stream);
+
 /* Bytes of DEVICE workspace dfa_plan_search needs (0 for bad sizes). */
 size_t dfa_plan_search_workspace_bytes(int n_layers, int B, int H, int L, int d);
 

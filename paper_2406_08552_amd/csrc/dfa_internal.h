@@ -35,6 +35,13 @@ struct ProjLaunch {
 
 hipError_t launch_mrae(const void* a, const void* b, size_t n, float eps, double* partial, int max_partials,
                        double* out, hipStream_t stream);
+// Workgroups (partial sums) of one MRAE reduction of n elements.
+size_t mrae_workgroups(size_t n, int max_partials);
+// Partial sums the allocation-free MRAE entry point keeps in device memory of
+// its own (a file-scope array of dfa_reduce.hip, one per device).
+constexpr int MRAE_SCRATCH_PARTIALS = 1024;
+// Device address of that array on the current device (looked up once per device).
+hipError_t scratch_partials(double** ptr);
 hipError_t launch_add_bf16(const void* a, const void* b, void* out, size_t n, hipStream_t stream);
 
 // Records the message returned by dfa_last_error() for a non-OK status.

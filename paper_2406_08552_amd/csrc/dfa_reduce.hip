@@ -5,9 +5,18 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "dfa_internal.h"
 
 namespace dfa {
+
+// Partial sums of the allocation-free MRAE entry point: one fp64 value per
+// workgroup of the reduction, 8 KiB, one copy per device, held until the
+// process ends.  In host code this name is only a stand-in for the symbol:
+// kernels get the device address that scratch_partials() looks up.
+static __device__ __align__(256) double scratch[MRAE_SCRATCH_PARTIALS];
+
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -95,16 +104,46 @@ __global__ void __launch_bounds__(256) add_bf16_kernel(const u32x4* a, const u32
 
 }  // namespace
 
-hipError_t launch_mrae(const void* a, const void* b, size_t n, float eps, double* partial, int max_partials,
-                       double* out, hipStream_t stream) {
+size_t mrae_workgroups(size_t n, int max_partials) {
     const size_t n8 = n / 8;
     size_t blocks = (n8 + MR_THREADS - 1) / MR_THREADS;
     if (blocks < 1) blocks = 1;
     if (blocks > (size_t)max_partials) blocks = (size_t)max_partials;
+    return blocks;
+}
+
+hipError_t launch_mrae(const void* a, const void* b, size_t n, float eps, double* partial, int max_partials,
+                       double* out, hipStream_t stream) {
+    const size_t blocks = mrae_workgroups(n, max_partials);
     hipLaunchKernelGGL(mrae_partial_kernel, dim3((unsigned)blocks), dim3(MR_THREADS), 0, stream, (const u32x4*)a,
                        (const u32x4*)b, n, eps, partial);
     hipLaunchKernelGGL(mrae_final_kernel, dim3(1), dim3(MR_THREADS), 0, stream, partial, (int)blocks, n, out);
     return hipGetLastError();
+}
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+double* g_scratch_ptr[MAX_DEVICES];
+}  // namespace
+
+// Device address of `scratch` on the calling thread's current device, looked
+// up once per device (with that device current) and kept.
+hipError_t scratch_partials(double** ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = (double*)p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_add_bf16(const void* a, const void* b, void* out, size_t n, hipStream_t stream) {

@@ -1,5 +1,5 @@
 // Host side of the plan search (Sec. 3.5, Alg. 1) and of the MRAE entry
-// point: the greedy loop runs on the host and drives the library's own
+// points: the greedy loop runs on the host and drives the library's own
 // module steps, residual adds and loss reduction on the GPU.
 #include <math.h>
 #include <stdint.h>
@@ -79,6 +79,22 @@ dfa_status dfa_mrae(const void* A, const void* B, size_t n, void* workspace, dou
         return err(DFA_ERR_INVALID_ARG, "dfa_mrae: A, B, workspace must be 16-byte aligned, result 8-byte aligned");
     return hip(dfa::launch_mrae(A, B, n, 1e-6f, (double*)workspace, DFA_MRAE_WORKSPACE_BYTES / sizeof(double), result,
                                 stream));
+}
+
+dfa_status dfa_mrae_noalloc(const void* A, const void* B, size_t n, double* result, hipStream_t stream) {
+    if (!A || !B || !result) return err(DFA_ERR_INVALID_ARG, "dfa_mrae_noalloc: NULL pointer");
+    if ((((uintptr_t)A | (uintptr_t)B) & 15) || ((uintptr_t)result & 7))
+        return err(DFA_ERR_INVALID_ARG, "dfa_mrae_noalloc: A and B must be 16-byte aligned, result 8-byte aligned");
+    if (n > DFA_MRAE_NOALLOC_MAX_ELEMS)
+        return err(DFA_ERR_INVALID_ARG, "dfa_mrae_noalloc: n exceeds DFA_MRAE_NOALLOC_MAX_ELEMS (2^40 elements)");
+    // the reduction's grid is capped at the array's length: one partial sum per workgroup
+    static_assert(MRAE_PARTIALS == dfa::MRAE_SCRATCH_PARTIALS, "same grid as dfa_mrae");
+    if (dfa::mrae_workgroups(n, MRAE_PARTIALS) > (size_t)dfa::MRAE_SCRATCH_PARTIALS)
+        return err(DFA_ERR_INVALID_ARG, "dfa_mrae_noalloc: more partial sums than the scratch array holds");
+    double* part = nullptr;
+    dfa_status st = hip(dfa::scratch_partials(&part));
+    if (st != DFA_OK) return st;
+    return hip(dfa::launch_mrae(A, B, n, 1e-6f, part, MRAE_PARTIALS, result, stream));
 }
 
 dfa_status dfa_plan_search(int n_layers, int n_steps, const void* const* X_steps, const void* const* Wqkv,

@@ -30,7 +30,7 @@ CODE_NAMES = {FULL: "FULL", WARS_REFRESH: "WARS_REFRESH", WARS_REUSE: "WARS_REUS
 # every symbol include/dfa.h declares
 EXPORTS = ("dfa_attn_full", "dfa_attn_full_and_residual", "dfa_attn_window_plus_residual",
            "dfa_plan_step", "dfa_plan_make", "dfa_qkv_proj", "dfa_out_proj", "dfa_module_step",
-           "dfa_mrae", "dfa_plan_search_workspace_bytes", "dfa_plan_search", "dfa_last_error", "dfa_version")
+           "dfa_mrae", "dfa_mrae_noalloc", "dfa_plan_search_workspace_bytes", "dfa_plan_search", "dfa_last_error", "dfa_version")
 MRAE_WORKSPACE_BYTES = 8192
 
 
@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
         L.dfa_module_step.restype = _int
         L.dfa_mrae.argtypes = [_vp, _vp, ctypes.c_size_t, _vp, _vp, _vp]
         L.dfa_mrae.restype = _int
+        L.dfa_mrae_noalloc.argtypes = [_vp, _vp, ctypes.c_size_t, _vp, _vp]
+        L.dfa_mrae_noalloc.restype = _int
         L.dfa_plan_search_workspace_bytes.argtypes = [_int] * 5
         L.dfa_plan_search_workspace_bytes.restype = ctypes.c_size_t
         _vpp = ctypes.POINTER(ctypes.c_void_p)
@@ -255,6 +257,18 @@ def dfa_mrae(A, B, workspace, result, stream=None) -> None:
     if _nbytes(workspace) < MRAE_WORKSPACE_BYTES or result.dtype != torch.float64 or result.numel() < 1:
         raise ValueError("workspace too small or result not an fp64 tensor")
     _check(lib().dfa_mrae(_ptr(A), _ptr(B), A.numel(), _ptr(workspace), _ptr(result), _stream(stream)))
+
+
+def dfa_mrae_noalloc(A, B, result, stream=None) -> None:
+    """dfa_mrae without a workspace: the library keeps the partial sums in a
+    device array of its own (no allocation by the call)."""
+    import torch
+    if A.dtype != torch.bfloat16 or B.dtype != torch.bfloat16 or A.numel() != B.numel():
+        raise ValueError("A and B must be bf16 tensors of the same size")
+    _on_gpu((A, "A"), (B, "B"), (result, "result"))
+    if result.dtype != torch.float64 or result.numel() < 1:
+        raise ValueError("result must be an fp64 tensor")
+    _check(lib().dfa_mrae_noalloc(_ptr(A), _ptr(B), A.numel(), _ptr(result), _stream(stream)))
 
 
 def plan_search_workspace_bytes(n_layers: int, B: int, H: int, L: int, d: int) -> int:

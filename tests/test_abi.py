@@ -187,6 +187,10 @@ def test_search_and_mrae_validation(L):
     assert L.dfa_mrae(None, 0x1000, 8, 0x2000, 0x3000, None) == dfa.DFA_ERR_INVALID_ARG
     assert L.dfa_mrae(0x1008, 0x1000, 8, 0x2000, 0x3000, None) == dfa.DFA_ERR_INVALID_ARG   # misaligned
     assert "aligned" in dfa.last_error()
+    assert L.dfa_mrae_noalloc(None, 0x1000, 8, 0x3000, None) == dfa.DFA_ERR_INVALID_ARG
+    assert L.dfa_mrae_noalloc(0x1000, 0x1000, 8, 0x3004, None) == dfa.DFA_ERR_INVALID_ARG   # misaligned result
+    assert L.dfa_mrae_noalloc(0x1000, 0x1000, (1 << 40) + 1, 0x3000, None) == dfa.DFA_ERR_INVALID_ARG
+    assert "2^40" in dfa.last_error()
     assert dfa.plan_search_workspace_bytes(3, 2, 2, 64, 64) > 0
     assert dfa.plan_search_workspace_bytes(0, 2, 2, 64, 64) == 0
     f = L.dfa_plan_search
