@@ -45,13 +45,15 @@ _vp, _int, _i32p = ctypes.c_void_p, ctypes.c_int, ctypes.POINTER(ctypes.c_int32)
 
 
 def lib() -> ctypes.CDLL:
-    """Load libdfa.so (built in-tree); raises if it has not been built."""
+    """Load libdfa.so (built in-tree; the environment variable DFA_LIBRARY
+    names another build of the same sources); raises if it is missing."""
     global _LIB
     if _LIB is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is missing: build it first "
+        path = os.environ.get("DFA_LIBRARY") or LIB_PATH
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it first "
                                "(python -c 'import __graft_entry__ as g; g.build()')")
-        L = ctypes.CDLL(LIB_PATH)
+        L = ctypes.CDLL(path)
         attn = [_vp, _vp, _vp, _vp, _vp, _int, _int, _int, _int, _int, _vp]
         for name in ("dfa_attn_full", "dfa_attn_full_and_residual", "dfa_attn_window_plus_residual"):
             f = getattr(L, name)
