@@ -488,6 +488,24 @@ __device__ __forceinline__ void issue_tile(const uint16_t* __restrict__ Kbh, con
     }
 }
 
+// Direct global -> LDS copy of n16 16-byte chunks starting at src (the
+// residual rows of a workgroup, at most NR chunks), chunk c landing at byte
+// 16 c of dst.  Addressed as a uniform base plus a 32-bit lane offset formed
+// here, so that no address stays live across the tile loop.
+template <int NR>
+__device__ __forceinline__ void issue_rows(const float* __restrict__ src, int n16, int tid, uint16_t* dst) {
+    const int wave_chunk0 = __builtin_amdgcn_readfirstlane(tid & ~63);
+    uint32_t off = (uint32_t)tid * 16u;
+    asm volatile("" : "+v"(off));
+#pragma unroll
+    for (int it = 0; it < (NR + NTHREADS - 1) / NTHREADS; ++it) {
+        if (it * NTHREADS + tid < n16)
+            __builtin_amdgcn_global_load_lds((const void*)((const char*)src + off + (uint32_t)(it * NTHREADS * 16)),
+                                             (__attribute__((address_space(3))) void*)(dst + 8 * (it * NTHREADS + wave_chunk0)),
+                                             16, 0, 0);
+    }
+}
+
 // Per-workgroup state of the tile walk.
 template <int D, int QB>
 struct Walk {
@@ -499,13 +517,20 @@ struct Walk {
     bool wave_active;
     float c;
     int stage;
+    // Residual rows copied into the free LDS stage while the last tile is
+    // used, so that the epilogue does not wait on their global read (null:
+    // none); rpre_n16 16-byte chunks.
+    const float* rpre;
+    int rpre_n16;
 
     // Visit tiles [t0, t1) with one segment kind; `next_after` is the first
     // tile of the next non-empty segment (-1: none), prefetched while the
     // last tile of this segment is used.
     template <int KIND, bool FINE = false>
     __device__ __forceinline__ void run(Acc<D, QB>& acc, const QFrag<D, QB>& q, int t0, int t1, int next_after) {
-        for (int t = t0; t < t1; ++t) {
+        // the walk's last tile is peeled when residual rows are to be copied
+        const int tl = (next_after < 0 && rpre) ? t1 - 1 : t1;
+        for (int t = t0; t < tl; ++t) {
             const uint16_t* Ks = smem + stage * G::STAGE_ELEMS;
             const uint16_t* Vs = Ks + G::KS_ELEMS;
             const int next = (t + 1 < t1) ? t + 1 : next_after;
@@ -514,6 +539,15 @@ struct Walk {
                 issue_tile<D>(Kbh, Vbh, next * BK, L, tid, Kn, Kn + G::KS_ELEMS);
             }
             if (wave_active) tile<KIND, FINE>(acc, q, Ks, Vs, t * BK);
+            wait_vm_all();
+            __syncthreads();
+            stage ^= 1;
+        }
+        if (tl < t1 && t0 < t1) {
+            const uint16_t* Ks = smem + stage * G::STAGE_ELEMS;
+            const uint16_t* Vs = Ks + G::KS_ELEMS;
+            issue_rows<bq<QB>() * D / 4>(rpre, rpre_n16, tid, smem + (stage ^ 1) * G::STAGE_ELEMS);
+            if (wave_active) tile<KIND, FINE>(acc, q, Ks, Vs, tl * BK);
             wait_vm_all();
             __syncthreads();
             stage ^= 1;
@@ -715,6 +749,17 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
     wk.wave_active = qw0 < L;
     wk.c = p.c;
     wk.stage = 0;
+    wk.rpre = nullptr;
+    wk.rpre_n16 = 0;
+    // 64-query window walks take their residual rows through the LDS stage
+    // that the last tile leaves free (one stage holds 64 fp32 rows of d <= 72)
+    if constexpr (MODE == MODE_WINDOW && QB == 1) {
+        static_assert(bq<1>() * D * 4 <= G::STAGE_ELEMS * 2, "residual rows must fit one LDS stage");
+        if (p.Rin) {
+            wk.rpre = p.Rin + head_off + (size_t)q0 * D;
+            wk.rpre_n16 = (min(L, q0 + bq<1>()) - q0) * D / 4;
+        }
+    }
 
     // segments of the tile walk
     const int ntiles = (L + BK - 1) / BK, nfull = L / BK;
@@ -829,7 +874,13 @@ __device__ __forceinline__ void attn_body(const Params& p, uint16_t* smem) {
                 *(f32x4*)(p.Rout + off) = o - win;
             }
             if constexpr (MODE == MODE_WINDOW) {
-                if (p.Rin) out = o + *(const f32x4*)(p.Rin + off);
+                if (wk.rpre) {
+                    // the walk's last iteration left the rows in the stage it freed
+                    const float* rl = (const float*)(smem + wk.stage * G::STAGE_ELEMS);
+                    out = o + *(const f32x4*)(rl + (qrow - q0) * D + col);
+                } else if (p.Rin) {
+                    out = o + *(const f32x4*)(p.Rin + off);
+                }
             }
             const u32x2 ov = u32x2{pack_bf16x2(out[0], out[1]), pack_bf16x2(out[2], out[3])};
             for (int di = 0; di < p.ndst; ++di) *(u32x2*)(p.dst[di] + off) = ov;
