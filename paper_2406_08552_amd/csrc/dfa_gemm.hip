@@ -19,10 +19,12 @@
 //
 // Work decomposition: a workgroup (4 wavefronts) owns 128 features x 128
 // or 256 tokens (the larger tile when the grid still has four rounds of work
-// per CU) and walks K in tiles of 64 or 32.  The next k-tile is loaded from
-// global memory into registers while the MFMAs consume the current one from
-// LDS, then stored into the other LDS buffer (double buffering, one barrier
-// per k-tile).  Each wavefront owns 64 features x 64 or 128 tokens as blocks
+// per CU) and walks K in tiles of 64 or 32.  The 128-token tile loads the
+// next k-tile from global memory into registers while the MFMAs consume the
+// current one from LDS, then stores it into the other LDS buffer (double
+// buffering, one barrier per k-tile).  The 256-token tile streams its k-tiles
+// through a ring of three LDS stages with direct global -> LDS copies issued
+// two k-tiles ahead (one barrier per k-tile, a partial vmcnt wait).  Each wavefront owns 64 features x 64 or 128 tokens as blocks
 // of v_mfma_f32_32x32x16_bf16 (operand layouts: lane l, h = l / 32, A element
 // e = A[l % 32][8h + e], B element e = B[8h + e][l % 32], output element
 // i = D[8 (i/4) + 4h + i%4][l % 32]).  The 128-token tile's LDS rows carry one
@@ -77,7 +79,12 @@ struct Tile {
     static constexpr int OP = GF + 8;                          // output staging row pitch (elements)
     static constexpr int ACH = GF * GCH / GT;                  // W chunks per thread and k-tile
     static constexpr int BCH = GTOK * GCH / GT;                // activation chunks per thread and k-tile
-    static constexpr int SMEM = 2 * STAGE > GTOK * OP ? 2 * STAGE : GTOK * OP;
+    // the 256-token tile streams its k-tiles through a ring of three LDS stages
+    // filled by direct global -> LDS copies two k-tiles ahead (RING); the
+    // 128-token tile stages them through registers into two LDS buffers
+    static constexpr bool RING = SHAPE == TILE_MANY;
+    static constexpr int NSTAGE = RING ? 3 : 2;
+    static constexpr int SMEM = NSTAGE * STAGE > GTOK * OP ? NSTAGE * STAGE : GTOK * OP;
     static_assert(GF * GCH % GT == 0 && GTOK * GCH % GT == 0, "chunks per thread");
     static_assert((size_t)SMEM * sizeof(uint16_t) * 2 <= 160 * 1024, "two workgroups per CU must fit in LDS");
 };
@@ -146,6 +153,41 @@ __device__ __forceinline__ void load_gemm_tile(const GemmParams& p, int n0, int 
     }
 }
 
+// Direct global -> LDS copy of k-tile kt into one stage (RING tiles): the
+// stage's 16-byte slots are filled in order, lane l of a copy writing slot
+// base + l, so each lane loads the chunk that the swizzle places in its slot
+// (slot P holds chunk (P & 3) ^ s(row) of row P >> 2).  Token rows beyond M
+// copy row M - 1 (their outputs are not stored).
+template <int ACT, int SHAPE>
+__device__ __forceinline__ void issue_gemm_tile(const GemmParams& p, int n0, int t0, int kt, int tid, uint16_t* As) {
+    using T = Tile<SHAPE>;
+    static_assert(T::SWZ && T::GCH == 4 && T::GP == 32, "ring tiles are swizzled 64-byte rows");
+    const int wave_slot0 = __builtin_amdgcn_readfirstlane(tid & ~63);
+#pragma unroll
+    for (int it = 0; it < T::ACH + T::BCH; ++it) {
+        const int slot = it * GT + tid;          // 16-byte slot of the stage (W rows first)
+        const int row = slot >> 2;
+        const int ch = (slot & 3) ^ (((row >> 1) & 2) | ((row >> 3) & 1));
+        const int kk = kt * T::GK + ch * 8;
+        const uint16_t* src;
+        if (row < GF) {
+            src = p.W + (size_t)(n0 + row) * p.K + kk;
+        } else {
+            const int t = min(t0 + row - GF, p.M - 1);
+            if constexpr (ACT == ACT_ROWS) {
+                src = p.act + (size_t)t * p.K + kk;
+            } else {
+                const int b = t / p.L, l = t - b * p.L;
+                const int h = kk / p.d, j = kk - h * p.d;
+                src = p.act + ((size_t)(b * p.H + h) * p.L + l) * p.d + j;
+            }
+        }
+        __builtin_amdgcn_global_load_lds((const void*)src,
+                                         (__attribute__((address_space(3))) void*)(As + 8 * (it * GT + wave_slot0)), 16, 0,
+                                         0);
+    }
+}
+
 template <int SHAPE>
 __device__ __forceinline__ void store_gemm_tile(int tid, const u32x4 (&r)[Tile<SHAPE>::ACH + Tile<SHAPE>::BCH],
                                                 uint16_t* As, uint16_t* Bs) {
@@ -187,6 +229,43 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
             for (int i = 0; i < 16; ++i) acc[mb][nb][i] = 0.f;
 
     const int nk = p.K / GK;
+    // one k-tile of MFMAs from LDS stage As / Bs
+    auto mma_tile = [&](const uint16_t* As, const uint16_t* Bs) {
+#pragma unroll
+        for (int ks = 0; ks < GK / 16; ++ks) {
+            const uint16_t* arow = As + chunk_off<SHAPE>(64 * wf + r32, 2 * ks + h);
+            const uint16_t* brow = Bs + chunk_off<SHAPE>(32 * BT * wt + r32, 2 * ks + h);
+            bf16x8 a[2], b[BT];
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) a[mb] = __builtin_bit_cast(bf16x8, *(const u32x4*)(arow + 32 * mb * GP));
+#pragma unroll
+            for (int nb = 0; nb < BT; ++nb) b[nb] = __builtin_bit_cast(bf16x8, *(const u32x4*)(brow + 32 * nb * GP));
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int nb = 0; nb < BT; ++nb)
+                    acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mb], b[nb], acc[mb][nb], 0, 0, 0);
+        }
+    };
+    if constexpr (T::RING) {
+        // k-tiles kt + 1 and kt + 2 are in flight while kt is used; each
+        // thread issues ACH + BCH copies per k-tile, so vmcnt(ACH + BCH)
+        // leaves only the newer k-tile outstanding
+        issue_gemm_tile<ACT, SHAPE>(p, n0, t0, 0, tid, smem);
+        if (nk > 1) issue_gemm_tile<ACT, SHAPE>(p, n0, t0, 1, tid, smem + T::STAGE);
+        for (int kt = 0; kt < nk; ++kt) {
+            static_assert(T::ACH + T::BCH < 16, "vmcnt immediate");
+            if (kt + 1 < nk) __builtin_amdgcn_s_waitcnt(0x0F70 | (T::ACH + T::BCH));
+            else __builtin_amdgcn_s_waitcnt(0x0F70);
+            // every copy of k-tile kt has landed, and every wavefront is done
+            // with the stage k-tile kt + 2 overwrites (the one k-tile kt - 1 used)
+            __syncthreads();
+            if (kt + 2 < nk) issue_gemm_tile<ACT, SHAPE>(p, n0, t0, kt + 2, tid, smem + ((kt + 2) % 3) * T::STAGE);
+            const uint16_t* As = smem + (kt % 3) * T::STAGE;
+            mma_tile(As, As + T::ATILE);
+        }
+        __syncthreads();
+    } else {
     int stage = 0;
     u32x4 stg[T::ACH + T::BCH];
     load_gemm_tile<ACT, SHAPE>(p, n0, t0, 0, tid, stg);
@@ -219,6 +298,7 @@ __global__ void __launch_bounds__(GT) __attribute__((amdgpu_waves_per_eu(2, 2)))
         }
         __syncthreads();
         stage ^= 1;
+    }
     }
 
     // epilogue: bias and bf16 rounding, then the tile goes through LDS as
