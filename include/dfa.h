@@ -30,10 +30,11 @@
  *            L-1.  w is the HALF-width; w >= L-1 covers every key.
  *   Numerics Scores and softmax statistics are fp32; the probabilities enter
  *            the PV product as bf16 and every accumulation is fp32.  Rows of
- *            at most 32 keys (windows with w <= 15, and every sequence of at
- *            most 32 tokens) add the bf16 rounding residual of each
- *            probability as a second PV operand: with so few keys the
- *            rounding of the weights does not average out.
+ *            at most 32 keys (windows with w <= 15, in window attention and in
+ *            the window pass of a refresh, and every sequence of at most 32
+ *            tokens) add the bf16 rounding residual of each probability as a
+ *            second PV operand: with so few keys the rounding of the weights
+ *            does not average out.
  *   CFG      A classifier-free-guidance batch holds B = 2P entries: entries
  *            0..P-1 are the conditional evaluations and entry b + P is the
  *            unconditional partner of entry b (Sec. 3.4).
@@ -45,10 +46,13 @@
  *   Streams  Every call is asynchronous on `stream` (0 = the null stream).
  *            Outputs are valid once the caller has synchronised the stream.
  *   Memory   The caller allocates and owns every buffer and the stream.  The
- *            library never allocates or frees and keeps no pointer after
+ *            library never allocates or frees (dfa_mrae_noalloc's array is a
+ *            static part of the library's device code) and keeps no pointer after
  *            returning; only dfa_plan_search synchronises (its stream, to read
- *            each trial's loss).  The one state kept between calls is the
- *            thread-local message of dfa_last_error().  Calls are re-entrant,
+ *            each trial's loss).  The state kept between calls is the
+ *            thread-local message of dfa_last_error() and, for
+ *            dfa_mrae_noalloc only, its fixed per-device scratch array (and
+ *            that array's address).  Calls are re-entrant,
  *            and calls on different streams may run concurrently as long as
  *            their output buffers do not overlap.
  *   Errors   Every function returns a dfa_status; nothing else crosses the
