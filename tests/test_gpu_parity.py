@@ -277,6 +277,60 @@ def test_rescale_paths(kind, L, d, w):
     check(f"{kind} window + R", O3, Wd + f64(Rres))
 
 
+# A bf16 pair whose score a * b lies just under the exact rescale threshold
+# 8 / c (c = log2(e) / sqrt(72) in fp32), while its probability against a
+# running max of 0, 2^(a b c - 7) (shifted by 2^-7 as the kernels form it),
+# rounds to 2.0 in bf16: the fast margin test of a plain tile then falls back
+# to the exact form, which finds no rescale and applies the tile with the
+# running max unchanged.
+MARGIN_A, MARGIN_B = 1.7421875, 27.0
+
+
+def test_rescale_margin_boundary():
+    """Plain tiles whose largest probability lands exactly on the margin bit
+    without exceeding the rescale threshold, in full attention and in the
+    plain segments of the refresh and window kernels (two query blocks per
+    wavefront, where the fast margin test runs)."""
+    c = np.float32(1.4426950408889634 / np.sqrt(72.0))
+    s = np.float32(MARGIN_A * MARGIN_B)
+    assert float(s) == MARGIN_A * MARGIN_B
+    thr = np.float32(np.float32(8.0) / c)
+    x = np.float32(np.float64(s) * np.float64(c) - 7.0)      # fma(s, c, -7), one rounding
+    p = float(np.float32(2.0 ** np.float64(x)))
+    assert s < thr and p < 2.0
+    assert float(torch.tensor(p).to(torch.bfloat16)) == 2.0
+    dev = torch.device("cuda")
+    B, H, L, d = 4, 16, 1152, 72                 # two query blocks per wavefront in all three kernels
+    shape = (B, H, L, d)
+    q = torch.zeros(shape)
+    q[..., 0] = MARGIN_A
+    k = torch.zeros(shape)
+    for h in range(H):
+        for t in range(1, L // 64, 2):           # odd tiles only: walks from an even tile start at max 0
+            k[:, h, 64 * t + (7 * t + 3 * h) % 64, 0] = MARGIN_B
+    v = torch.randn(shape, generator=torch.Generator().manual_seed(77)).to(torch.bfloat16)
+    q, k = q.to(torch.bfloat16), k.to(torch.bfloat16)
+    rows = inputs.sample_rows(L, 64, 99)
+    Qd, Kd, Vd = f64(q), f64(k), f64(v)
+    gq, gk, gv = (t.to(dev) for t in (q, k, v))
+    O = torch.empty(shape, dtype=torch.bfloat16, device=dev)
+    R = torch.empty(shape, dtype=torch.float32, device=dev)
+    say("margin boundary: full")
+    dfa.dfa_attn_full(gq, gk, gv, O, 100)
+    torch.cuda.synchronize()
+    Of = orc.attention_rows(Qd, Kd, Vd, rows)
+    check("margin full", O.cpu(), Of, rows)
+    say("margin boundary: refresh w=100")
+    dfa.dfa_attn_full_and_residual(gq, gk, gv, O, R, 100)
+    torch.cuda.synchronize()
+    check("margin refresh O", O.cpu(), Of, rows)
+    check("margin refresh R", R.cpu(), Of - orc.attention_rows(Qd, Kd, Vd, rows, 100), rows)
+    say("margin boundary: window w=700")
+    dfa.dfa_attn_window_plus_residual(gq, gk, gv, O, None, 700)
+    torch.cuda.synchronize()
+    check("margin window", O.cpu(), orc.attention_rows(Qd, Kd, Vd, rows, 700), rows)
+
+
 @pytest.mark.parametrize("B,H,L,d,w", [
     (3, 2, 1236, 64, 1),    # three keys per query: the bf16 rounding of the weights alone passed the bound
     (2, 4, 1500, 72, 2),
