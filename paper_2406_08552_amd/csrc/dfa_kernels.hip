@@ -101,7 +101,10 @@ constexpr float RESCALE_THRESH = 8.0f;    // lazy rescale margin (log2 units)
 // Probabilities are formed as 2^(x - m - P_SHIFT): a probability at the rescale
 // margin is then exactly 2, the smallest value whose bf16 form has the top
 // exponent bit set, so one OR over the packed probabilities tests the margin.
-// The power-of-two factor cancels in O / l and commutes with every rounding.
+// The power-of-two factor cancels in O / l.  The shifted exponent argument is
+// rounded at a larger magnitude, which moves any probability of at least 2^-8
+// of the running max by at most about 2^-21 of itself, far below its bf16
+// rounding.
 constexpr float P_SHIFT = RESCALE_THRESH - 1.0f;
 constexpr uint32_t P_MARGIN_BITS = 0x40004000u;   // top exponent bit of both packed bf16 values
 constexpr int FINE_MAX_HALF_WIDTH = 15;   // window half-widths applied with split probabilities
