@@ -237,6 +237,58 @@ def test_concurrent_streams_match_serial():
         assert torch.equal(a, b), "concurrent streams changed a result"
 
 
+def test_plan_graph_replay():
+    """A plan pass captured in a HIP graph (every plan code, a separate output
+    cache so that AST launches its copy, tiled and short-sequence layers)
+    replays to the same bits as the same pass run eagerly, on every replay:
+    the state is reset and other eager work runs between replays."""
+    dev = torch.device("cuda")
+    # one query block per wavefront (d = 64, one-pass refresh), two blocks (the fast update), short sequences
+    layers = [((2, 2, 300, 64), 40, [dfa.WARS_REFRESH, dfa.WARS_REUSE, dfa.AST_REUSE, dfa.ASC_REUSE,
+                                      dfa.WARS_ASC_REFRESH, dfa.WARS_ASC_REUSE, dfa.FULL, dfa.WARS_REUSE]),
+              ((4, 16, 1100, 72), 700, [dfa.FULL, dfa.WARS_REFRESH, dfa.AST_REUSE, dfa.WARS_REUSE,
+                                        dfa.WARS_ASC_REFRESH, dfa.ASC_REUSE, dfa.WARS_ASC_REUSE, dfa.WARS_REUSE]),
+              ((4, 2, 24, 72), 3, [dfa.WARS_REFRESH, dfa.ASC_REUSE, dfa.WARS_REUSE, dfa.AST_REUSE,
+                                   dfa.WARS_ASC_REFRESH, dfa.WARS_ASC_REUSE, dfa.FULL, dfa.AST_REUSE])]
+    qkv = [tuple(t.to(dev) for t in rand_qkv(shape, 500 + i)) for i, (shape, _, _) in enumerate(layers)]
+    state = [(torch.zeros(shape, dtype=torch.bfloat16, device=dev), torch.zeros(shape, dtype=torch.float32, device=dev),
+              torch.zeros(shape, dtype=torch.bfloat16, device=dev)) for shape, _, _ in layers]
+    snapshot = [tuple(t.clone() for t in st) for st in state]
+
+    def plan_pass():
+        for t in range(8):
+            for (shape, w, codes), (q, k, v), (O, R, C) in zip(layers, qkv, state):
+                dfa.dfa_plan_step(codes[t], q, k, v, O, R, C, w)
+
+    def reset():
+        for st, sn in zip(state, snapshot):
+            for a, b in zip(st, sn):
+                a.copy_(b)
+
+    say("graph replay: eager reference")
+    reset()
+    plan_pass()
+    torch.cuda.synchronize()
+    ref = [tuple(t.clone() for t in st) for st in state]
+    reset()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        plan_pass()
+    other = torch.empty(layers[0][0], dtype=torch.bfloat16, device=dev)
+    for i in range(3):
+        say(f"graph replay {i}")
+        reset()
+        q, k, v = qkv[0]
+        dfa.dfa_attn_full(q, k, v, other, 0)          # the program's own eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for li, (st, rf) in enumerate(zip(state, ref)):
+            for name, a, b in zip("ORC", st, rf):
+                assert torch.equal(a, b), f"replay {i}: layer {li} {name} differs from the eager pass"
+
+
 @pytest.mark.parametrize("kind,L,d,w", [("large", 2048, 72, 300), ("growing", 2048, 72, 300),
                                          ("growing", 1000, 64, 77), ("large", 777, 64, 0),
                                          ("growing", 500, 72, 40), ("large", 300, 64, 0),
