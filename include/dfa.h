@@ -45,6 +45,9 @@
  *            projection and module entry points.
  *   Streams  Every call is asynchronous on `stream` (0 = the null stream).
  *            Outputs are valid once the caller has synchronised the stream.
+ *            The attention, plan-step, projection and module calls only
+ *            launch kernels (no copy, memset or synchronisation), so they may
+ *            be captured into a HIP graph on `stream` and replayed.
  *   Memory   The caller allocates and owns every buffer and the stream.  The
  *            library never allocates or frees (dfa_mrae_noalloc's array is a
  *            static part of the library's device code) and keeps no pointer after
