@@ -315,8 +315,10 @@ def module_bench(args, cfg, dfa, inputs, torch, dev, stream, code, kres):
     M = B * L
     qkv_flops, out_flops = 2.0 * M * C * 3 * C, 2.0 * M * C * C
     reps = args.kernel_reps
-    ms_qkv = timed(torch, stream, lambda: dfa.dfa_qkv_proj(X[0], Wqkv, bqkv, Q, K, V, stream), reps)
-    ms_out = timed(torch, stream, lambda: dfa.dfa_out_proj(O, Wo, bo, Y[0], stream), reps)
+    # timed like the attention kernels: interleaved rounds, median per entry point
+    proj = interleaved(torch, stream, {"qkv": lambda: dfa.dfa_qkv_proj(X[0], Wqkv, bqkv, Q, K, V, stream),
+                                       "out": lambda: dfa.dfa_out_proj(O, Wo, bo, Y[0], stream)}, reps)
+    ms_qkv, ms_out = proj["qkv"], proj["out"]
 
     def step(c, l):
         dfa.dfa_module_step(c, X[l], Wqkv, bqkv, Wo, bo, Q, K, V, O, R[l], Y[l], Y[l], w, H, stream)
