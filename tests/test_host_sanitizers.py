@@ -5,7 +5,7 @@ UndefinedBehaviorSanitizer, running the ABI tests on the CPU.
 The host sources are compiled by g++ with the sanitizers; the HIP sources are
 compiled as usual (no sanitizer reaches device code) and linked in, so the
 library is complete.  The ABI tests run in a child process that preloads the
-ASan runtime and loads this build through DFA_LIBRARY; any sanitizer report
+ASan runtime and loads the sanitized library through DFA_LIBRARY; any sanitizer report
 makes the child fail (halt on the first error, no recovery)."""
 import hashlib
 import os
