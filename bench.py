@@ -392,7 +392,8 @@ def cpu_baseline(cfg, target_s: float):
     attention takes about target_s / 4 seconds of host work; `value` is that
     full-attention rate in TFLOP/s.  Then the oracle's sampled plan step runs
     one layer-step per plan code (refresh, reuse, ASC, full, AST) on a quarter
-    of those rows, each timed in ms."""
+    of those rows (on every row where they cost little: the short DiT
+    shapes), each timed in ms."""
     import numpy as np
 
     from oracle import dfa_oracle as orc
@@ -422,8 +423,10 @@ def cpu_baseline(cfg, target_s: float):
         if elapsed >= target_s / 4 or n_rows >= L:
             break
         n_rows = min(L, n_rows * 4 if elapsed < target_s / 16 else n_rows * 2)
-    # one layer-step per code on a quarter of those rows (bounds the host time)
-    code_rows = inputs.sample_rows(L, max(16, len(rows) // 4), 4)
+    # one layer-step per code on a quarter of those rows (bounds the host time),
+    # or on every row when all of them took under a sixteenth of the budget
+    all_rows = len(rows) == L and elapsed < target_s / 16
+    code_rows = np.arange(L) if all_rows else inputs.sample_rows(L, max(16, len(rows) // 4), 4)
     per_code = {}
     cache = orc.LayerCache()
     for c in (orc.WARS_REFRESH, orc.WARS_REUSE, orc.ASC_REUSE, orc.FULL, orc.AST_REUSE):
