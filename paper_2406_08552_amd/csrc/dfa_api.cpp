@@ -142,7 +142,7 @@ extern "C" {
 
 const char* dfa_last_error(void) { return g_last_error.c_str(); }
 
-const char* dfa_version(void) { return "0.5.0"; }
+const char* dfa_version(void) { return "0.6.0"; }
 
 dfa_status dfa_attn_full(const void* Q, const void* K, const void* V, void* O, void* R, int B, int H, int L, int d,
                          int w, hipStream_t stream) {
