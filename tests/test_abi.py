@@ -223,3 +223,17 @@ def test_binding_rejects_host_tensors():
     q = torch.zeros((1, 1, 64, 64), dtype=torch.bfloat16)
     with pytest.raises(ValueError, match="GPU"):
         dfa.dfa_attn_full(q, q, q, q.clone(), 0)
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """With no built library the binding raises on first use; there is no
+    fallback path (checked in a fresh interpreter pointed at a missing file)."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("from paper_2406_08552_amd import dfa\n"
+            "try:\n    dfa.lib()\nexcept RuntimeError as e:\n    print('raised:', e)\n")
+    env = dict(os.environ, DFA_LIBRARY=str(tmp_path / "libdfa_missing.so"))
+    out = subprocess.run([sys.executable, "-c", code], cwd=root, env=env, capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stderr
+    assert "raised:" in out.stdout and "is missing" in out.stdout, out.stdout
